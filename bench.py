@@ -1,0 +1,189 @@
+#!/usr/bin/env python
+"""Throughput of the hindsight re-scoring hot path on one MI355X.
+
+One step = the whole path over one batch of synthetic inputs already resident
+in HBM: both contexts' teacher-forced log-probabilities of every eligible
+token through the fused lm-head kernel (hdl_token_logprobs), then the
+divergence score and per-root top-k (hdl_select_branch_points).
+
+Default workload: 8 roots x 2 contexts, T=4096, d=2048, V=151936, bf16, the
+first 32 positions of each root excluded, k=8.
+
+Prints one JSON line:  value = scored tokens/s (both contexts), plus the
+fused kernel's roofline (achieved TFLOP/s of algorithmic 2*d*V flops per
+scored token over its HIP-event-timed duration, against the 2.5 PFLOP/s
+dense bf16 MFMA peak) and the float64 oracle timed on a bounded sample on
+the host cores.
+"""
+from __future__ import annotations
+
+import argparse
+import json
+import os
+import sys
+import time
+
+ROOT = os.path.dirname(os.path.abspath(__file__))
+if ROOT not in sys.path:
+    sys.path.insert(0, ROOT)
+
+PEAK_TFLOPS = {"bf16": 2500.0, "f32": 157.3}   # MI355X dense MFMA (fp32: matrix fp32 peak)
+METRIC = "scored tokens/sec (both contexts) + MFMA util of fused lm-head logprob kernel"
+
+
+def log(msg: str) -> None:
+    print(f"[bench] {msg}", file=sys.stderr, flush=True)
+
+
+def cpu_baseline(w, budget_s: float = 15.0, max_rows: int = 4096):
+    """Time the float64 oracle on a seeded sample of eligible rows (both
+    contexts) on the host cores; return oracle scored tokens/s."""
+    import numpy as np
+    import torch
+    from oracle import hdl_oracle as O
+    try:
+        from threadpoolctl import threadpool_info
+        cores = max([int(i.get("num_threads", 1)) for i in threadpool_info() if i.get("user_api") == "blas"] or [1])
+    except Exception:  # pragma: no cover - informational only
+        cores = os.cpu_count() or 1
+    c = w.cfg
+    if c.dtype == "bf16":
+        Wd = O.bf16_bits_to_f64(w.W.view(torch.int16).numpy().view(np.uint16))
+    else:
+        Wd = w.W.double().numpy()
+    hidden = w.rows_hidden()
+    tokens = w.rows_tokens().numpy()
+    elig = np.nonzero(w.rows_mask().numpy())[0]
+    rng = np.random.default_rng(12345)
+    sample = rng.permutation(elig)[:max_rows]
+    done, t_total, blk = 0, 0.0, 64
+    while done < len(sample) and t_total < budget_s:
+        rows = np.sort(sample[done:done + blk])
+        if c.dtype == "bf16":
+            H = O.bf16_bits_to_f64(hidden[torch.as_tensor(rows)].view(torch.int16).numpy().view(np.uint16))
+        else:
+            H = hidden[torch.as_tensor(rows)].double().numpy()
+        t0 = time.perf_counter()
+        O.token_logprobs(H, Wd, tokens[rows])
+        t_total += time.perf_counter() - t0
+        done += len(rows)
+    return {"value": done / t_total, "unit": "scored tokens/s", "cores": cores, "kind": "oracle",
+            "sample": f"{done} eligible rows drawn from both contexts of this workload "
+                      f"(float64 lm-head log-softmax, {t_total:.1f} s)"}
+
+
+def main() -> int:
+    ap = argparse.ArgumentParser()
+    ap.add_argument("--gpus", type=int, default=1)
+    ap.add_argument("--steps", type=int, default=20)
+    ap.add_argument("--warmup", type=int, default=3)
+    ap.add_argument("--workload", default="c2", help="tiny | c2 | c3 | c4 | c5 (default c2)")
+    ap.add_argument("--no-cpu-baseline", action="store_true")
+    ap.add_argument("--cpu-budget", type=float, default=15.0)
+    args = ap.parse_args()
+
+    if args.gpus != 1 or int(os.environ.get("WORLD_SIZE", "1")) != 1:
+        print("bench.py measures one GPU only: this build has no multi-GPU path "
+              "(rows are independent; sharding is described in the design notes).", file=sys.stderr)
+        return 2
+
+    import numpy as np
+    import torch
+
+    import paper_2609_36864_amd as hdl
+    import workloads
+
+    if not torch.cuda.is_available():
+        print("bench.py needs a GPU", file=sys.stderr)
+        return 2
+    hdl.load_library()
+    dev = torch.device("cuda:0")
+
+    t0 = time.time()
+    w = workloads.make_workload(args.workload)
+    c = w.cfg
+    log(f"generated workload {args.workload} in {time.time() - t0:.1f} s")
+
+    hidden = w.rows_hidden().to(dev)
+    W = w.W.to(dev)
+    tokens = w.rows_tokens().to(dev)
+    mask = w.rows_mask().to(dev)
+    mask_rt = w.mask.to(dev)
+    n_rows = hidden.shape[0]
+    n_scored = int(mask.sum().item())
+    dt = hdl.HDL_BF16 if c.dtype == "bf16" else hdl.HDL_F32
+    ws = torch.empty(hdl.workspace_size(n_rows, c.d, c.V, dt), dtype=torch.uint8, device=dev)
+    logp = torch.empty(n_rows, dtype=torch.float32, device=dev)
+    torch.cuda.synchronize()
+    log(f"inputs resident on {torch.cuda.get_device_name(0)}: {n_rows} rows, {n_scored} scored")
+
+    def step():
+        hdl.token_logprobs(hidden, W, tokens, mask, logp=logp, want_lse=False, workspace=ws)
+        lp = logp.view(2, c.R, c.T)
+        return hdl.select_branch_points(lp[0], lp[1], mask_rt, c.k)
+
+    for _ in range(args.warmup):
+        step()
+    torch.cuda.synchronize()
+    log(f"warmup done ({args.warmup} steps)")
+
+    hdl.profile_enable(True)
+    hdl.profile_read()   # reset the tally
+    ev0 = torch.cuda.Event(enable_timing=True)
+    ev1 = torch.cuda.Event(enable_timing=True)
+    torch.cuda.synchronize()
+    t_start = time.perf_counter()
+    ev0.record()
+    for _ in range(args.steps):
+        out = step()
+    ev1.record()
+    torch.cuda.synchronize()
+    wall = time.perf_counter() - t_start
+    kern_ms, launches = hdl.profile_read()
+    hdl.profile_enable(False)
+    step_ms = ev0.elapsed_time(ev1) / args.steps
+    log(f"timed {args.steps} steps: {step_ms:.3f} ms/step (wall {wall / args.steps * 1e3:.3f} ms/step), "
+        f"fused kernel {kern_ms / max(launches, 1):.3f} ms/launch")
+
+    idx, score, count, _ = out
+    counts = count.cpu().numpy()
+    if not (np.all(counts == min(c.k, c.T)) or np.all(counts <= c.k)):
+        raise RuntimeError("selection produced an invalid count")
+    if not torch.isfinite(logp[mask.bool()]).all():
+        raise RuntimeError("non-finite log-probabilities")
+
+    value = n_scored / (step_ms / 1e3)
+    flops = 2.0 * c.d * c.V * n_scored
+    kern_avg_ms = kern_ms / max(launches, 1)
+    achieved = flops / (kern_avg_ms / 1e3) / 1e12
+    peak = PEAK_TFLOPS[c.dtype]
+    result = {
+        "metric": METRIC,
+        "value": value,
+        "unit": "scored tokens/s",
+        "n_gpus": 1,
+        "steps": args.steps,
+        "warmup": args.warmup,
+        "ms_per_step": step_ms,
+        "higher_is_better": True,
+        "scaling": "weak",
+        "vs_baseline": None,
+        "dtype": c.dtype,
+        "data": "synthetic (seeded generator; random lm-head weights and hidden states)",
+        "config": {"workload": f"{args.workload}: {workloads.DESCRIPTIONS[args.workload]}",
+                   "roots": c.R, "T": c.T, "d": c.d, "V": c.V, "k": c.k,
+                   "scored_tokens_per_step": n_scored},
+        "roofline": {"bound": "mfma", "achieved": achieved, "peak": peak, "unit": "TFLOP/s",
+                     "frac": achieved / peak, "traffic": None,
+                     "kernel": "lmhead_logprob_kernel", "kernel_ms": kern_avg_ms,
+                     "flops_per_launch": flops},
+    }
+    if not args.no_cpu_baseline:
+        log("timing the float64 oracle on a bounded sample")
+        result["cpu_baseline"] = cpu_baseline(w, budget_s=args.cpu_budget)
+    print(json.dumps(result), flush=True)
+    return 0
+
+
+if __name__ == "__main__":
+    sys.exit(main())

@@ -1,0 +1,147 @@
+/*
+ * hdl.h -- C ABI of libhdl.so, the MI355X (gfx950) hindsight re-scoring path
+ * of Hindsight-Divergence Localization (HDL).
+ *
+ * The paper re-scores each sampled root twice with teacher forcing, once
+ * under the original context and once under the hindsight context (Sec. 3.1,
+ * Eq. 1), scores every policy-generated token by the absolute change of its
+ * log-likelihood (Sec. 3.2, Eq. 2) and keeps the highest-scoring positions of
+ * each root as branch points (Sec. 3.2; two per root in Sec. 4.1).
+ *
+ * Conventions shared by every entry point
+ *  - All array pointers are DEVICE pointers to caller-owned memory.  The
+ *    library allocates no device memory and keeps no pointer after a call
+ *    returns.
+ *  - Work is enqueued asynchronously on `stream` (a hipStream_t; NULL means
+ *    the default stream).  Outputs are valid once the caller synchronises the
+ *    stream.  The library never synchronises.
+ *  - Argument errors are reported synchronously by a negative return value,
+ *    before anything is enqueued.  A failed kernel launch returns
+ *    HDL_ERR_HIP.  hdl_last_error() describes the most recent failure of the
+ *    calling thread.  No C++ exception crosses this boundary.
+ *  - Row-major layouts throughout; "[a, b]" means a rows of b contiguous
+ *    elements.
+ */
+#ifndef HDL_H_
+#define HDL_H_
+
+#include <stddef.h>
+#include <stdint.h>
+
+#ifdef __cplusplus
+extern "C" {
+#endif
+
+/* Element type of `hidden` and `w_vocab`.  Accumulation, the log-sum-exp and
+ * all outputs are fp32 for both. */
+typedef enum { HDL_F32 = 0, HDL_BF16 = 1 } hdl_dtype;
+
+enum {
+  HDL_OK = 0,
+  HDL_ERR_INVALID_ARG = -1, /* null pointer, non-positive size, bad alignment */
+  HDL_ERR_UNSUPPORTED = -2, /* unknown dtype, d not a multiple of 8, k > 1024 */
+  HDL_ERR_WORKSPACE = -3,   /* workspace missing or smaller than required    */
+  HDL_ERR_HIP = -4          /* a HIP call or kernel launch failed            */
+};
+
+/* Largest k accepted by hdl_select_branch_points. */
+#define HDL_MAX_K 1024
+
+/*
+ * Bytes of device workspace hdl_token_logprobs needs for these sizes
+ * (0 if the sizes are invalid).  The workspace holds the compacted list of
+ * scored rows and the per-vocabulary-chunk partial log-sum-exp states.
+ */
+size_t hdl_token_logprobs_workspace_size(int64_t n_rows, int64_t d, int64_t vocab,
+                                         int dtype);
+
+/*
+ * Teacher-forced log-likelihood of each row's sampled token (Eq. 1):
+ *
+ *     logp[n] = z_n[tokens[n]] - log sum_v exp(z_n[v]),   z_n = W_vocab h_n,
+ *
+ * computed by one fused kernel: the lm-head contraction on bf16 (or fp32)
+ * MFMA tiles with fp32 accumulation, an online max / log-sum-exp carried
+ * across vocabulary tiles, and capture of the sampled token's logit.  The
+ * n_rows x vocab logits are never written to memory.
+ *
+ *  hidden   [n_rows, d]  dtype; row n is the final hidden state that PREDICTS
+ *                        tokens[n] (the caller applies the teacher-forcing
+ *                        shift).  For HDL both contexts go in one call, rows
+ *                        ordered [context][root][t]; W is shared (Eq. 1 uses
+ *                        the same parameters for both contexts).  16-byte
+ *                        aligned.
+ *  w_vocab  [vocab, d]   dtype, the lm-head weight (nn.Linear layout).
+ *                        16-byte aligned.
+ *  tokens   [n_rows]     int32 sampled tokens.  Precondition: 0 <= t < vocab;
+ *                        a row that violates it gets logp = NaN (never an
+ *                        error).
+ *  mask     [n_rows]     uint8, or NULL for "all rows".  Only rows with
+ *                        mask != 0 (policy-generated tokens, Sec. 3.1) are
+ *                        computed; the others get logp = 0 and lse = 0 and
+ *                        cost no matrix work.
+ *  d                     multiple of 8.
+ *  logp     [n_rows]     fp32 out.
+ *  lse_out  [n_rows]     fp32 out (log-sum-exp of the row), or NULL.
+ *  workspace             device memory of at least
+ *                        hdl_token_logprobs_workspace_size(...) bytes,
+ *                        256-byte aligned; contents on entry are ignored.
+ *
+ * Deterministic: the same inputs give bitwise-identical outputs, and a row's
+ * result does not depend on the other rows of the call.
+ */
+int hdl_token_logprobs(const void* hidden, const void* w_vocab, const int32_t* tokens,
+                       const uint8_t* mask, int64_t n_rows, int64_t d, int64_t vocab,
+                       int dtype, float* logp, float* lse_out, void* workspace,
+                       size_t workspace_bytes, void* stream);
+
+/*
+ * Hindsight-divergence score and per-root branch-point selection (Eq. 2 and
+ * the ranking of Sec. 3.2):
+ *
+ *     s[r, t] = | logp_hind[r, t] - logp_orig[r, t] |     (fp32 subtraction)
+ *
+ * over eligible positions (mask != 0 and a finite difference; NaN rows never
+ * qualify).  For each root the k eligible positions with the largest s are
+ * returned ordered by (s descending, t ascending); an exact tie at the k-th
+ * place goes to the lower t.
+ *
+ *  logp_orig, logp_hind [n_roots, T] fp32, as written by hdl_token_logprobs.
+ *  mask         [n_roots, T] uint8, or NULL for "all positions".
+ *  k            1 .. HDL_MAX_K.
+ *  idx          [n_roots, k] int32 out: selected positions, -1 padding.
+ *  score        [n_roots, k] fp32 out: their s, 0 padding.
+ *  count        [n_roots]    int32 out: min(k, number of eligible positions).
+ *  delta_signed [n_roots, T] fp32 out (logp_hind - logp_orig on eligible
+ *               positions, 0 elsewhere), or NULL.
+ */
+int hdl_select_branch_points(const float* logp_orig, const float* logp_hind,
+                             const uint8_t* mask, int64_t n_roots, int64_t T, int32_t k,
+                             int32_t* idx, float* score, int32_t* count,
+                             float* delta_signed, void* stream);
+
+/* Static description of a status code. */
+const char* hdl_status_string(int status);
+
+/* Description of the calling thread's most recent failure ("" if none). */
+const char* hdl_last_error(void);
+
+/* ABI version of this library (increments on incompatible changes). */
+int hdl_abi_version(void);
+
+/*
+ * Kernel timing for measurement tools.  While enabled, every
+ * hdl_token_logprobs call brackets its fused lm-head kernel with HIP events
+ * on the caller's stream.  hdl_profile_read waits for those events, returns
+ * the summed kernel time in milliseconds and the number of launches since
+ * the last read, and resets the tally.  Disabled by default; enabling adds
+ * two event records per call.  Not thread-safe.
+ */
+int hdl_profile_enable(int on);
+int hdl_profile_read(double* total_ms, int64_t* launches);
+
+#ifdef __cplusplus
+}
+#endif
+
+#endif /* HDL_H_ */

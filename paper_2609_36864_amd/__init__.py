@@ -1,0 +1,220 @@
+"""MI355X (gfx950) hindsight re-scoring path of Hindsight-Divergence Localization.
+
+A thin ctypes binding over libhdl.so (C ABI in include/hdl.h).  Every step of
+the path runs in the library's HIP kernels; this module only checks tensor
+arguments, allocates outputs and workspace with torch, and passes device
+pointers and the current HIP stream.  There is no CPU fallback: without the
+built library or a GPU the calls raise.
+
+    logp, lse = token_logprobs(hidden, w_vocab, tokens, mask)          # Eq. 1
+    idx, score, count, delta = select_branch_points(lp0, lpH, mask, k)  # Eq. 2
+"""
+from __future__ import annotations
+
+import ctypes
+import os
+from typing import Optional, Tuple
+
+import torch
+
+__all__ = ["HdlError", "HDL_F32", "HDL_BF16", "HDL_MAX_K", "library_path", "load_library",
+           "workspace_size", "token_logprobs", "select_branch_points", "rescore",
+           "profile_enable", "profile_read", "abi_version"]
+
+HDL_F32 = 0
+HDL_BF16 = 1
+HDL_MAX_K = 1024
+
+_PKG_DIR = os.path.dirname(os.path.abspath(__file__))
+_LIB: Optional[ctypes.CDLL] = None
+
+
+class HdlError(RuntimeError):
+    def __init__(self, status: int, message: str):
+        super().__init__(f"libhdl status {status}: {message}")
+        self.status = status
+
+
+def library_path() -> str:
+    return os.path.join(_PKG_DIR, "libhdl.so")
+
+
+def load_library() -> ctypes.CDLL:
+    """Load libhdl.so (built by paper_2609_36864_amd.build); raises if absent."""
+    global _LIB
+    if _LIB is not None:
+        return _LIB
+    path = library_path()
+    if not os.path.exists(path):
+        raise RuntimeError(f"{path} is not built; run `python -m paper_2609_36864_amd.build`")
+    L = ctypes.CDLL(path)
+    c_i64, c_vp, c_sz = ctypes.c_int64, ctypes.c_void_p, ctypes.c_size_t
+    L.hdl_token_logprobs_workspace_size.argtypes = [c_i64, c_i64, c_i64, ctypes.c_int]
+    L.hdl_token_logprobs_workspace_size.restype = c_sz
+    L.hdl_token_logprobs.argtypes = [c_vp, c_vp, c_vp, c_vp, c_i64, c_i64, c_i64, ctypes.c_int,
+                                     c_vp, c_vp, c_vp, c_sz, c_vp]
+    L.hdl_token_logprobs.restype = ctypes.c_int
+    L.hdl_select_branch_points.argtypes = [c_vp, c_vp, c_vp, c_i64, c_i64, ctypes.c_int32,
+                                           c_vp, c_vp, c_vp, c_vp, c_vp]
+    L.hdl_select_branch_points.restype = ctypes.c_int
+    L.hdl_status_string.argtypes = [ctypes.c_int]
+    L.hdl_status_string.restype = ctypes.c_char_p
+    L.hdl_last_error.argtypes = []
+    L.hdl_last_error.restype = ctypes.c_char_p
+    L.hdl_abi_version.argtypes = []
+    L.hdl_abi_version.restype = ctypes.c_int
+    L.hdl_profile_enable.argtypes = [ctypes.c_int]
+    L.hdl_profile_enable.restype = ctypes.c_int
+    L.hdl_profile_read.argtypes = [ctypes.POINTER(ctypes.c_double), ctypes.POINTER(c_i64)]
+    L.hdl_profile_read.restype = ctypes.c_int
+    _LIB = L
+    return L
+
+
+def _check(status: int) -> None:
+    if status != 0:
+        L = load_library()
+        msg = L.hdl_last_error().decode() or L.hdl_status_string(status).decode()
+        raise HdlError(status, msg)
+
+
+def _ptr(t: Optional[torch.Tensor]) -> Optional[int]:
+    return None if t is None else t.data_ptr()
+
+
+def _stream_handle(device: torch.device) -> int:
+    return torch.cuda.current_stream(device).cuda_stream
+
+
+def _require_cuda(name: str, t: torch.Tensor) -> None:
+    if not isinstance(t, torch.Tensor) or t.device.type != "cuda":
+        raise ValueError(f"{name} must be a CUDA (HIP) tensor")
+    if not t.is_contiguous():
+        raise ValueError(f"{name} must be contiguous")
+
+
+def abi_version() -> int:
+    return int(load_library().hdl_abi_version())
+
+
+def workspace_size(n_rows: int, d: int, vocab: int, dtype: int) -> int:
+    return int(load_library().hdl_token_logprobs_workspace_size(n_rows, d, vocab, dtype))
+
+
+_WS_CACHE: dict = {}
+
+
+def _workspace(device: torch.device, nbytes: int) -> torch.Tensor:
+    key = (device.index, str(torch.cuda.current_stream(device)))
+    ws = _WS_CACHE.get(key)
+    if ws is None or ws.numel() < nbytes:
+        ws = torch.empty(max(nbytes, 256), dtype=torch.uint8, device=device)
+        _WS_CACHE[key] = ws
+    return ws
+
+
+def token_logprobs(hidden: torch.Tensor, w_vocab: torch.Tensor, tokens: torch.Tensor,
+                   mask: Optional[torch.Tensor] = None, *, logp: Optional[torch.Tensor] = None,
+                   lse: Optional[torch.Tensor] = None, want_lse: bool = True,
+                   workspace: Optional[torch.Tensor] = None) -> Tuple[torch.Tensor, Optional[torch.Tensor]]:
+    """Teacher-forced log p of each row's sampled token (Eq. 1), fused lm-head.
+
+    hidden [n_rows, d] and w_vocab [vocab, d], both bf16 or both fp32;
+    tokens [n_rows] int32; mask [n_rows] uint8/bool or None.
+    Returns (logp [n_rows] fp32, lse [n_rows] fp32 or None).
+    """
+    L = load_library()
+    for name, t in (("hidden", hidden), ("w_vocab", w_vocab), ("tokens", tokens)):
+        _require_cuda(name, t)
+    if hidden.dim() != 2 or w_vocab.dim() != 2 or hidden.shape[1] != w_vocab.shape[1]:
+        raise ValueError("hidden must be [n_rows, d] and w_vocab [vocab, d]")
+    if hidden.dtype != w_vocab.dtype or hidden.dtype not in (torch.bfloat16, torch.float32):
+        raise ValueError("hidden and w_vocab must both be bfloat16 or both float32")
+    if tokens.dtype != torch.int32 or tokens.shape != (hidden.shape[0],):
+        raise ValueError("tokens must be int32 [n_rows]")
+    n_rows, d = hidden.shape
+    vocab = w_vocab.shape[0]
+    dev = hidden.device
+    if mask is not None:
+        _require_cuda("mask", mask)
+        if mask.dtype == torch.bool:
+            mask = mask.view(torch.uint8)
+        if mask.dtype != torch.uint8 or mask.shape != (n_rows,):
+            raise ValueError("mask must be uint8 [n_rows]")
+    dt = HDL_BF16 if hidden.dtype == torch.bfloat16 else HDL_F32
+    if logp is None:
+        logp = torch.empty(n_rows, dtype=torch.float32, device=dev)
+    if want_lse and lse is None:
+        lse = torch.empty(n_rows, dtype=torch.float32, device=dev)
+    nbytes = workspace_size(n_rows, d, vocab, dt)
+    if nbytes == 0:
+        raise ValueError(f"invalid sizes n_rows={n_rows} d={d} vocab={vocab}")
+    ws = workspace if workspace is not None else _workspace(dev, nbytes)
+    _check(L.hdl_token_logprobs(hidden.data_ptr(), w_vocab.data_ptr(), tokens.data_ptr(), _ptr(mask),
+                                n_rows, d, vocab, dt, logp.data_ptr(), _ptr(lse), ws.data_ptr(),
+                                ws.numel() * ws.element_size(), _stream_handle(dev)))
+    return logp, lse
+
+
+def select_branch_points(logp_orig: torch.Tensor, logp_hind: torch.Tensor,
+                         mask: Optional[torch.Tensor], k: int, *, want_delta: bool = False):
+    """|Delta log p| (Eq. 2) and the per-root top-k branch points (Sec. 3.2).
+
+    logp_orig, logp_hind [R, T] fp32; mask [R, T] uint8 or None.
+    Returns (idx [R,k] int32, score [R,k] fp32, count [R] int32, delta [R,T] or None).
+    """
+    L = load_library()
+    _require_cuda("logp_orig", logp_orig)
+    _require_cuda("logp_hind", logp_hind)
+    if logp_orig.dtype != torch.float32 or logp_hind.dtype != torch.float32:
+        raise ValueError("log-probabilities must be float32")
+    if logp_orig.dim() != 2 or logp_orig.shape != logp_hind.shape:
+        raise ValueError("logp_orig and logp_hind must both be [R, T]")
+    R, T = logp_orig.shape
+    dev = logp_orig.device
+    if mask is not None:
+        _require_cuda("mask", mask)
+        if mask.dtype == torch.bool:
+            mask = mask.view(torch.uint8)
+        if mask.dtype != torch.uint8 or tuple(mask.shape) != (R, T):
+            raise ValueError("mask must be uint8 [R, T]")
+    kk = max(int(k), 1)
+    idx = torch.empty(R, kk, dtype=torch.int32, device=dev)
+    score = torch.empty(R, kk, dtype=torch.float32, device=dev)
+    count = torch.empty(R, dtype=torch.int32, device=dev)
+    delta = torch.empty(R, T, dtype=torch.float32, device=dev) if want_delta else None
+    _check(L.hdl_select_branch_points(logp_orig.data_ptr(), logp_hind.data_ptr(), _ptr(mask), R, T,
+                                      int(k), idx.data_ptr(), score.data_ptr(), count.data_ptr(),
+                                      _ptr(delta), _stream_handle(dev)))
+    return idx, score, count, delta
+
+
+def rescore(hidden_both: torch.Tensor, w_vocab: torch.Tensor, tokens: torch.Tensor,
+            mask: Optional[torch.Tensor], k: int, *, workspace: Optional[torch.Tensor] = None):
+    """The whole hot path for R roots: both contexts' log-probs in one fused
+    call, then the divergence score and per-root top-k.
+
+    hidden_both [2, R, T, d] (original context first), tokens [R, T] int32,
+    mask [R, T] uint8 or None.  Returns (logp [2, R, T], idx, score, count).
+    """
+    _, R, T, d = hidden_both.shape
+    rows = hidden_both.reshape(2 * R * T, d)
+    tok2 = tokens.reshape(1, R * T).expand(2, R * T).reshape(-1)
+    m2 = None if mask is None else mask.reshape(1, R * T).expand(2, R * T).reshape(-1)
+    logp, _ = token_logprobs(rows, w_vocab, tok2.contiguous(), None if m2 is None else m2.contiguous(),
+                             want_lse=False, workspace=workspace)
+    lp = logp.view(2, R, T)
+    idx, score, count, _ = select_branch_points(lp[0], lp[1], mask, k)
+    return lp, idx, score, count
+
+
+def profile_enable(on: bool = True) -> None:
+    _check(load_library().hdl_profile_enable(1 if on else 0))
+
+
+def profile_read() -> Tuple[float, int]:
+    """(summed fused-kernel milliseconds, launches) since the last read."""
+    ms = ctypes.c_double(0.0)
+    n = ctypes.c_int64(0)
+    _check(load_library().hdl_profile_read(ctypes.byref(ms), ctypes.byref(n)))
+    return float(ms.value), int(n.value)

@@ -1,0 +1,231 @@
+// Host side of libhdl.so: argument validation, work planning, workspace
+// layout and kernel launches behind the C ABI declared in include/hdl.h.
+#include <hip/hip_runtime.h>
+
+#include <cstdarg>
+#include <cstdint>
+#include <cstdio>
+#include <cstring>
+#include <mutex>
+#include <vector>
+
+#include "../../include/hdl.h"
+#include "hdl_internal.h"
+
+namespace {
+
+thread_local char g_last_error[512] = "";
+
+int fail(int status, const char* fmt, ...) __attribute__((format(printf, 2, 3)));
+int fail(int status, const char* fmt, ...) {
+  va_list ap;
+  va_start(ap, fmt);
+  std::vsnprintf(g_last_error, sizeof(g_last_error), fmt, ap);
+  va_end(ap);
+  return status;
+}
+
+int hip_fail(hipError_t e, const char* what) {
+  return fail(HDL_ERR_HIP, "%s: %s", what, hipGetErrorString(e));
+}
+
+bool aligned(const void* p, size_t a) { return (reinterpret_cast<uintptr_t>(p) % a) == 0; }
+
+size_t round_up(size_t x, size_t a) { return (x + a - 1) / a * a; }
+
+// ---- kernel timing (measurement tools only) ------------------------------
+struct Profiler {
+  std::mutex mu;
+  bool on = false;
+  std::vector<std::pair<hipEvent_t, hipEvent_t>> pending;
+  std::vector<std::pair<hipEvent_t, hipEvent_t>> spare;
+};
+Profiler g_prof;
+
+}  // namespace
+
+namespace hdl {
+
+LmheadPlan make_plan(int64_t n_rows, int64_t vocab) {
+  LmheadPlan p{};
+  p.n_rows = n_rows;
+  p.n_vt = (vocab + kTileV - 1) / kTileV;
+  p.n_rt_max = (n_rows + kTileN - 1) / kTileN;
+  // Vocabulary tiles per work item: long items amortise the per-item merge
+  // and partial write; short ones balance the tail across 256 CUs.  Aim for
+  // at least ~2048 items when the problem allows.
+  int64_t tpc = (p.n_rt_max * p.n_vt) / 2048;
+  if (tpc < 1) tpc = 1;
+  if (tpc > 16) tpc = 16;
+  p.tpc = tpc;
+  p.n_ch = (p.n_vt + tpc - 1) / tpc;
+  p.n_grt = (p.n_rt_max + kGroupRT - 1) / kGroupRT;
+  p.n_gch = (p.n_ch + kGroupCH - 1) / kGroupCH;
+  const int64_t groups = p.n_grt * p.n_gch;
+  p.grid = (groups + kNumXcd - 1) / kNumXcd * kNumXcd * (kGroupRT * kGroupCH);
+  // workspace: rows [n_rows] | n_scored + block counts | partials [3][n_ch][n_rows]
+  size_t off = 0;
+  p.off_rows = off;
+  off = round_up(off + sizeof(int32_t) * static_cast<size_t>(n_rows), 256);
+  p.off_count = off;
+  const size_t n_blocks = static_cast<size_t>((n_rows + 4095) / 4096);
+  off = round_up(off + sizeof(int32_t) * (64 + n_blocks), 256);
+  p.off_part = off;
+  off = round_up(off + 3 * sizeof(float) * static_cast<size_t>(p.n_ch) * static_cast<size_t>(n_rows), 256);
+  p.bytes = off;
+  return p;
+}
+
+}  // namespace hdl
+
+extern "C" {
+
+size_t hdl_token_logprobs_workspace_size(int64_t n_rows, int64_t d, int64_t vocab, int dtype) {
+  if (n_rows <= 0 || d <= 0 || vocab <= 0 || n_rows > INT32_MAX || vocab > INT32_MAX) return 0;
+  if (dtype != HDL_F32 && dtype != HDL_BF16) return 0;
+  return hdl::make_plan(n_rows, vocab).bytes;
+}
+
+int hdl_token_logprobs(const void* hidden, const void* w_vocab, const int32_t* tokens,
+                       const uint8_t* mask, int64_t n_rows, int64_t d, int64_t vocab, int dtype,
+                       float* logp, float* lse_out, void* workspace, size_t workspace_bytes,
+                       void* stream) {
+  g_last_error[0] = '\0';
+  if (!hidden || !w_vocab || !tokens || !logp)
+    return fail(HDL_ERR_INVALID_ARG, "hdl_token_logprobs: null hidden, w_vocab, tokens or logp");
+  if (n_rows <= 0 || d <= 0 || vocab <= 0)
+    return fail(HDL_ERR_INVALID_ARG, "hdl_token_logprobs: sizes must be positive (n_rows=%lld d=%lld vocab=%lld)",
+                static_cast<long long>(n_rows), static_cast<long long>(d), static_cast<long long>(vocab));
+  if (n_rows > INT32_MAX || vocab > INT32_MAX)
+    return fail(HDL_ERR_UNSUPPORTED, "hdl_token_logprobs: n_rows and vocab must fit in int32");
+  if (dtype != HDL_F32 && dtype != HDL_BF16)
+    return fail(HDL_ERR_UNSUPPORTED, "hdl_token_logprobs: unknown dtype %d", dtype);
+  if (d % 8 != 0)
+    return fail(HDL_ERR_UNSUPPORTED, "hdl_token_logprobs: d=%lld is not a multiple of 8", static_cast<long long>(d));
+  if (!aligned(hidden, 16) || !aligned(w_vocab, 16))
+    return fail(HDL_ERR_INVALID_ARG, "hdl_token_logprobs: hidden and w_vocab must be 16-byte aligned");
+  const hdl::LmheadPlan plan = hdl::make_plan(n_rows, vocab);
+  if (!workspace || workspace_bytes < plan.bytes)
+    return fail(HDL_ERR_WORKSPACE, "hdl_token_logprobs: workspace of %zu bytes needed, %zu given",
+                plan.bytes, workspace ? workspace_bytes : static_cast<size_t>(0));
+  if (!aligned(workspace, 256))
+    return fail(HDL_ERR_INVALID_ARG, "hdl_token_logprobs: workspace must be 256-byte aligned");
+  if (plan.grid > INT32_MAX)
+    return fail(HDL_ERR_UNSUPPORTED, "hdl_token_logprobs: problem too large for one launch");
+
+  hipStream_t s = static_cast<hipStream_t>(stream);
+  char* ws = static_cast<char*>(workspace);
+  int32_t* rows = reinterpret_cast<int32_t*>(ws + plan.off_rows);
+  int32_t* n_scored = reinterpret_cast<int32_t*>(ws + plan.off_count);
+  float* part = reinterpret_cast<float*>(ws + plan.off_part);
+  const size_t plane = static_cast<size_t>(plan.n_ch) * static_cast<size_t>(n_rows);
+
+  hipError_t e = hdl::launch_compact(mask, n_rows, rows, n_scored, logp, lse_out, s);
+  if (e != hipSuccess) return hip_fail(e, "compaction launch");
+
+  hdl::LmheadArgs a{};
+  a.hidden = hidden;
+  a.w = w_vocab;
+  a.tokens = tokens;
+  a.rows = rows;
+  a.n_scored = n_scored;
+  a.d = d;
+  a.vocab = vocab;
+  a.n_vt = plan.n_vt;
+  a.tpc = plan.tpc;
+  a.n_ch = plan.n_ch;
+  a.n_grt = plan.n_grt;
+  a.part_stride = n_rows;
+  a.part_m = part;
+  a.part_s = part + plane;
+  a.part_z = part + 2 * plane;
+
+  std::pair<hipEvent_t, hipEvent_t> ev{nullptr, nullptr};
+  bool timed = false;
+  {
+    std::lock_guard<std::mutex> lk(g_prof.mu);
+    if (g_prof.on) {
+      if (!g_prof.spare.empty()) {
+        ev = g_prof.spare.back();
+        g_prof.spare.pop_back();
+      } else if (hipEventCreate(&ev.first) != hipSuccess || hipEventCreate(&ev.second) != hipSuccess) {
+        return fail(HDL_ERR_HIP, "hdl_token_logprobs: hipEventCreate failed");
+      }
+      timed = true;
+    }
+  }
+  if (timed && (e = hipEventRecord(ev.first, s)) != hipSuccess) return hip_fail(e, "hipEventRecord");
+  e = hdl::launch_lmhead(a, plan.grid, dtype == HDL_BF16, s);
+  if (e != hipSuccess) return hip_fail(e, "lm-head kernel launch");
+  if (timed) {
+    if ((e = hipEventRecord(ev.second, s)) != hipSuccess) return hip_fail(e, "hipEventRecord");
+    std::lock_guard<std::mutex> lk(g_prof.mu);
+    g_prof.pending.push_back(ev);
+  }
+  e = hdl::launch_merge(a, n_rows, logp, lse_out, s);
+  if (e != hipSuccess) return hip_fail(e, "merge kernel launch");
+  return HDL_OK;
+}
+
+int hdl_select_branch_points(const float* logp_orig, const float* logp_hind, const uint8_t* mask,
+                             int64_t n_roots, int64_t T, int32_t k, int32_t* idx, float* score,
+                             int32_t* count, float* delta_signed, void* stream) {
+  g_last_error[0] = '\0';
+  if (!logp_orig || !logp_hind || !idx || !score || !count)
+    return fail(HDL_ERR_INVALID_ARG, "hdl_select_branch_points: null required pointer");
+  if (n_roots <= 0 || T <= 0)
+    return fail(HDL_ERR_INVALID_ARG, "hdl_select_branch_points: n_roots and T must be positive");
+  if (k < 1)
+    return fail(HDL_ERR_INVALID_ARG, "hdl_select_branch_points: k=%d must be >= 1", k);
+  if (k > HDL_MAX_K)
+    return fail(HDL_ERR_UNSUPPORTED, "hdl_select_branch_points: k=%d exceeds %d", k, HDL_MAX_K);
+  if (n_roots > INT32_MAX || T > INT32_MAX)
+    return fail(HDL_ERR_UNSUPPORTED, "hdl_select_branch_points: n_roots and T must fit in int32");
+  hipError_t e = hdl::launch_select(logp_orig, logp_hind, mask, n_roots, T, k, idx, score, count,
+                                    delta_signed, static_cast<hipStream_t>(stream));
+  if (e != hipSuccess) return hip_fail(e, "selection kernel launch");
+  return HDL_OK;
+}
+
+const char* hdl_status_string(int status) {
+  switch (status) {
+    case HDL_OK: return "ok";
+    case HDL_ERR_INVALID_ARG: return "invalid argument";
+    case HDL_ERR_UNSUPPORTED: return "unsupported argument";
+    case HDL_ERR_WORKSPACE: return "workspace missing or too small";
+    case HDL_ERR_HIP: return "HIP error";
+    default: return "unknown status";
+  }
+}
+
+const char* hdl_last_error(void) { return g_last_error; }
+
+int hdl_abi_version(void) { return 1; }
+
+int hdl_profile_enable(int on) {
+  std::lock_guard<std::mutex> lk(g_prof.mu);
+  g_prof.on = on != 0;
+  return HDL_OK;
+}
+
+int hdl_profile_read(double* total_ms, int64_t* launches) {
+  std::lock_guard<std::mutex> lk(g_prof.mu);
+  double tot = 0.0;
+  int64_t n = 0;
+  for (auto& ev : g_prof.pending) {
+    hipError_t e = hipEventSynchronize(ev.second);
+    if (e != hipSuccess) return hip_fail(e, "hipEventSynchronize");
+    float ms = 0.f;
+    e = hipEventElapsedTime(&ms, ev.first, ev.second);
+    if (e != hipSuccess) return hip_fail(e, "hipEventElapsedTime");
+    tot += ms;
+    ++n;
+    g_prof.spare.push_back(ev);
+  }
+  g_prof.pending.clear();
+  if (total_ms) *total_ms = tot;
+  if (launches) *launches = n;
+  return HDL_OK;
+}
+
+}  // extern "C"

@@ -1,0 +1,197 @@
+// Hindsight-divergence score and per-root branch-point selection (Eq. 2 and
+// the ranking of Sec. 3.2).
+//
+// One 1024-thread workgroup per root.  For position t:
+//     delta = logp_hind[t] - logp_orig[t]   (one fp32 subtraction)
+//     s     = |delta|,  eligible = mask[t] != 0 and delta finite.
+// The k largest s are found by a radix select on the bits of s (a
+// non-negative float orders like its bit pattern): four 8-bit digits, most
+// significant first, each resolved from an LDS histogram.  That yields the
+// threshold score S and how many positions at exactly S are needed; those
+// are the lowest-indexed ties (a scan in position order).  The kk <= 1024
+// winners are then sorted by the composite key (s, ~t) with a bitonic sort
+// in LDS, giving the order (s descending, t ascending).
+#include "hdl_internal.h"
+
+namespace hdl {
+namespace {
+
+constexpr int kThreads = 1024;
+constexpr int kWaves = kThreads / 64;
+
+struct Scratch {
+  int wsum[kWaves];
+  int hist[256];
+  int digit;
+  int rank;
+  unsigned long long keys[kThreads];
+};
+
+__device__ __forceinline__ int wave_incl_scan(int v) {
+  const int lane = threadIdx.x & 63;
+#pragma unroll
+  for (int o = 1; o < 64; o <<= 1) {
+    const int u = __shfl_up(v, o);
+    if (lane >= o) v += u;
+  }
+  return v;
+}
+
+// Exclusive block scan; *total receives the block sum.  Contains barriers:
+// every thread of the block must call it.
+__device__ __forceinline__ int block_excl_scan(int v, int* total, Scratch& sh) {
+  const int incl = wave_incl_scan(v);
+  const int w = threadIdx.x >> 6;
+  if ((threadIdx.x & 63) == 63) sh.wsum[w] = incl;
+  __syncthreads();
+  int before = 0, all = 0;
+#pragma unroll
+  for (int i = 0; i < kWaves; ++i) {
+    const int x = sh.wsum[i];
+    before += (i < w) ? x : 0;
+    all += x;
+  }
+  __syncthreads();
+  *total = all;
+  return before + incl - v;
+}
+
+struct Pos {
+  float delta;
+  unsigned key;
+  bool elig;
+};
+
+__device__ __forceinline__ Pos load_pos(const float* lo, const float* lh, const uint8_t* mask,
+                                        int64_t base, int64_t t) {
+  Pos p;
+  const float d = lh[base + t] - lo[base + t];
+  const bool on = (mask == nullptr) || (mask[base + t] != 0);
+  p.elig = on && __builtin_isfinite(d);
+  p.delta = p.elig ? d : 0.f;
+  p.key = __float_as_uint(__builtin_fabsf(p.delta));
+  return p;
+}
+
+__global__ __launch_bounds__(kThreads) void select_kernel(const float* __restrict__ lo,
+                                                          const float* __restrict__ lh,
+                                                          const uint8_t* __restrict__ mask,
+                                                          int64_t T, int k,
+                                                          int32_t* __restrict__ idx,
+                                                          float* __restrict__ score,
+                                                          int32_t* __restrict__ count,
+                                                          float* __restrict__ delta_out) {
+  __shared__ Scratch sh;
+  const int r = blockIdx.x;
+  const int tid = threadIdx.x;
+  const int64_t base = static_cast<int64_t>(r) * T;
+
+  // ---- eligibility count (and the optional signed delta) -----------------
+  int c = 0;
+  for (int64_t t = tid; t < T; t += kThreads) {
+    const Pos p = load_pos(lo, lh, mask, base, t);
+    if (delta_out) delta_out[base + t] = p.delta;
+    c += p.elig ? 1 : 0;
+  }
+  int n_elig;
+  block_excl_scan(c, &n_elig, sh);
+  const int kk = n_elig < k ? n_elig : k;
+
+  if (kk > 0) {
+    // ---- radix select of the kk-th largest score --------------------------
+    unsigned prefix = 0, pmask = 0;
+    int rank = kk;   // rank of the threshold among positions matching prefix
+    for (int shift = 24; shift >= 0; shift -= 8) {
+      for (int i = tid; i < 256; i += kThreads) sh.hist[i] = 0;
+      __syncthreads();
+      for (int64_t t = tid; t < T; t += kThreads) {
+        const Pos p = load_pos(lo, lh, mask, base, t);
+        if (p.elig && (p.key & pmask) == prefix) atomicAdd(&sh.hist[(p.key >> shift) & 255], 1);
+      }
+      __syncthreads();
+      // Inclusive scan over bins from the top digit down; the bin in which
+      // the running count reaches `rank` holds the threshold.
+      const int h = (tid < 256) ? sh.hist[255 - tid] : 0;
+      int tot;
+      const int above = block_excl_scan(h, &tot, sh);
+      if (tid < 256 && above < rank && above + h >= rank) {
+        sh.digit = 255 - tid;
+        sh.rank = rank - above;
+      }
+      __syncthreads();
+      prefix |= static_cast<unsigned>(sh.digit) << shift;
+      pmask |= 255u << shift;
+      rank = sh.rank;
+      __syncthreads();
+    }
+    const unsigned thr = prefix;   // bit pattern of the kk-th largest score
+    const int need_ties = rank;    // positions scoring exactly thr to take
+
+    // ---- collect: all above the threshold, then the lowest-indexed ties ---
+    int ties_before = 0, filled = 0;
+    for (int64_t t0 = 0; t0 < T; t0 += kThreads) {
+      const int64_t t = t0 + tid;
+      Pos p;
+      if (t < T) p = load_pos(lo, lh, mask, base, t);
+      else { p.elig = false; p.key = 0; p.delta = 0.f; }
+      const bool eq = p.elig && p.key == thr;
+      int n_eq;
+      const int tie_rank = ties_before + block_excl_scan(eq ? 1 : 0, &n_eq, sh);
+      const bool take = p.elig && (p.key > thr || (eq && tie_rank < need_ties));
+      int n_take;
+      const int slot = filled + block_excl_scan(take ? 1 : 0, &n_take, sh);
+      if (take && slot < kThreads)
+        sh.keys[slot] = (static_cast<unsigned long long>(p.key) << 32) |
+                        static_cast<unsigned long long>(0xFFFFFFFFu - static_cast<unsigned>(t));
+      ties_before += n_eq;
+      filled += n_take;
+    }
+    __syncthreads();
+
+    // ---- bitonic sort, descending, of the kk winners ----------------------
+    int P = 1;
+    while (P < kk) P <<= 1;
+    for (int i = kk + tid; i < P; i += kThreads) sh.keys[i] = 0ull;
+    __syncthreads();
+    for (int size = 2; size <= P; size <<= 1) {
+      for (int stride = size >> 1; stride > 0; stride >>= 1) {
+        for (int i = tid; i < P; i += kThreads) {
+          const int jx = i ^ stride;
+          if (jx > i) {
+            const unsigned long long a = sh.keys[i], bb = sh.keys[jx];
+            const bool desc = (i & size) == 0;
+            if (desc ? (a < bb) : (a > bb)) {
+              sh.keys[i] = bb;
+              sh.keys[jx] = a;
+            }
+          }
+        }
+        __syncthreads();
+      }
+    }
+  }
+
+  for (int j = tid; j < k; j += kThreads) {
+    if (j < kk) {
+      const unsigned long long key = sh.keys[j];
+      idx[static_cast<int64_t>(r) * k + j] = static_cast<int32_t>(0xFFFFFFFFu - static_cast<unsigned>(key & 0xFFFFFFFFull));
+      score[static_cast<int64_t>(r) * k + j] = __uint_as_float(static_cast<unsigned>(key >> 32));
+    } else {
+      idx[static_cast<int64_t>(r) * k + j] = -1;
+      score[static_cast<int64_t>(r) * k + j] = 0.f;
+    }
+  }
+  if (tid == 0) count[r] = kk;
+}
+
+}  // namespace
+
+hipError_t launch_select(const float* lo, const float* lh, const uint8_t* mask, int64_t n_roots,
+                         int64_t T, int k, int32_t* idx, float* score, int32_t* count, float* delta,
+                         hipStream_t stream) {
+  hipLaunchKernelGGL(select_kernel, dim3(static_cast<unsigned>(n_roots)), dim3(kThreads), 0, stream,
+                     lo, lh, mask, T, k, idx, score, count, delta);
+  return hipGetLastError();
+}
+
+}  // namespace hdl

@@ -1,0 +1,79 @@
+"""The C ABI without a GPU: the library loads, exports every function that
+include/hdl.h declares, and rejects bad arguments synchronously (argument
+checks run before any HIP call)."""
+import ctypes
+import os
+import re
+
+import pytest
+
+import paper_2609_36864_amd as hdl
+
+ROOT = os.path.dirname(os.path.dirname(os.path.abspath(__file__)))
+HEADER = os.path.join(ROOT, "include", "hdl.h")
+
+
+def _declared_functions():
+    src = open(HEADER).read()
+    src = re.sub(r"/\*.*?\*/", "", src, flags=re.S)
+    return sorted(set(re.findall(r"\b(hdl_[a-z0-9_]+)\s*\(", src)))
+
+
+@pytest.fixture(scope="module")
+def lib():
+    if not os.path.exists(hdl.library_path()):
+        pytest.fail("libhdl.so is not built (run __graft_entry__.build())")
+    return hdl.load_library()
+
+
+def test_header_declares_the_boundary():
+    names = _declared_functions()
+    for n in ("hdl_token_logprobs", "hdl_select_branch_points", "hdl_token_logprobs_workspace_size",
+              "hdl_status_string", "hdl_last_error"):
+        assert n in names
+
+
+def test_every_declared_symbol_is_exported(lib):
+    for n in _declared_functions():
+        assert hasattr(lib, n), f"{n} declared in hdl.h but not exported"
+
+
+def test_status_strings(lib):
+    assert lib.hdl_status_string(0) == b"ok"
+    for s in (-1, -2, -3, -4):
+        assert lib.hdl_status_string(s) not in (b"ok", b"unknown status")
+    assert lib.hdl_abi_version() == 1
+
+
+def test_workspace_size_rules(lib):
+    f = lib.hdl_token_logprobs_workspace_size
+    assert f(0, 64, 100, 1) == 0 and f(10, 0, 100, 1) == 0 and f(10, 64, 0, 1) == 0
+    assert f(10, 64, 100, 7) == 0
+    a = f(1000, 64, 151936, 1)
+    b = f(100000, 64, 151936, 1)
+    assert 0 < a < b
+    assert f(65536, 2048, 151936, 1) % 256 == 0
+
+
+def test_logprobs_argument_errors(lib):
+    call = lib.hdl_token_logprobs
+    p = ctypes.c_void_p(4096)       # never dereferenced: validation fails first
+    assert call(None, p, p, None, 4, 64, 10, 1, p, None, p, 1 << 20, None) == -1
+    assert b"null" in lib.hdl_last_error()
+    assert call(p, p, p, None, 0, 64, 10, 1, p, None, p, 1 << 20, None) == -1
+    assert call(p, p, p, None, 4, 64, 10, 5, p, None, p, 1 << 20, None) == -2
+    assert call(p, p, p, None, 4, 12, 10, 1, p, None, p, 1 << 20, None) == -2
+    assert call(ctypes.c_void_p(4100), p, p, None, 4, 64, 10, 1, p, None, p, 1 << 20, None) == -1
+    assert call(p, p, p, None, 4, 64, 10, 1, p, None, p, 16, None) == -3
+    assert call(p, p, p, None, 4, 64, 10, 1, p, None, None, 1 << 20, None) == -3
+    assert call(p, p, p, None, 4, 64, 10, 1, p, None, ctypes.c_void_p(4096 + 128), 1 << 20, None) == -1
+
+
+def test_select_argument_errors(lib):
+    call = lib.hdl_select_branch_points
+    p = ctypes.c_void_p(4096)
+    assert call(None, p, None, 1, 10, 2, p, p, p, None, None) == -1
+    assert call(p, p, None, 0, 10, 2, p, p, p, None, None) == -1
+    assert call(p, p, None, 1, 10, 0, p, p, p, None, None) == -1
+    assert call(p, p, None, 1, 10, 1025, p, p, p, None, None) == -2
+    assert b"1025" in lib.hdl_last_error()

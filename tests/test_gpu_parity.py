@@ -1,0 +1,280 @@
+"""GPU parity of the fused lm-head log-probability path (Eq. 1) and of the
+divergence / top-k selection (Eq. 2, Sec. 3.2) against the float64 oracle,
+element by element, through the C ABI.
+
+Tolerances: |log p error| <= 2e-3 for bf16 inputs (the stated bar) and
+<= 1e-4 for fp32 inputs (fp32 accumulation over d <= 256 and a vocabulary
+of 4096 errs by ~1e-6; 1e-4 leaves margin for the exp2/log2 hardware
+approximations).  Selection is integer work and is compared bit-exactly on
+identical fp32 inputs; end to end, branch sets follow the tie-tolerant rule.
+"""
+import math
+
+import numpy as np
+import pytest
+import torch
+
+import workloads
+from oracle import hdl_oracle as O
+from tests.gpu_helpers import as_f64, flat_inputs, oracle_rows, require_gpu, run_logprobs
+
+pytestmark = pytest.mark.gpu
+
+TOL_BF16 = 2e-3
+TOL_F32 = 1e-4
+
+
+@pytest.fixture(scope="module")
+def hdl():
+    return require_gpu()
+
+
+def _check_all_rows(hdl, w, tol):
+    hidden, W, tokens, mask = flat_inputs(w)
+    lp, lse = run_logprobs(hdl, hidden, W, tokens, mask)
+    m = mask.numpy().astype(bool)
+    rows = np.nonzero(m)[0]
+    want, want_lse = oracle_rows(hidden, W, tokens, rows)
+    err = np.abs(lp[rows] - want)
+    assert err.max() <= tol, f"max |logp err| {err.max():.3g} at row {rows[err.argmax()]}"
+    assert np.abs(lse[rows] - want_lse).max() <= tol
+    assert np.all(lp[~m] == 0.0) and np.all(lse[~m] == 0.0)
+    assert np.all(lp <= 0.0)
+    return lp, want, rows
+
+
+def test_tiny_full_parity_and_branch_points(hdl):
+    w = workloads.make_workload("tiny")
+    lp, want, rows = _check_all_rows(hdl, w, TOL_F32)
+    T, k = w.cfg.T, w.cfg.k
+    dev = "cuda"
+    lp_t = torch.from_numpy(lp).to(dev)
+    m = w.mask.to(dev)
+    idx, score, count, delta = hdl.select_branch_points(lp_t[:T].view(1, T), lp_t[T:].view(1, T), m, k,
+                                                        want_delta=True)
+    torch.cuda.synchronize()
+    # oracle ranking from oracle log-probs: the gap at k is huge here, so the
+    # branch set and its order must match exactly
+    full = np.zeros(2 * T)
+    full[rows] = want
+    oi, osc, oc = O.select_branch_points(full[:T][None], full[T:][None], w.mask.numpy(), k)
+    assert idx.cpu().numpy().tolist() == oi.tolist()
+    assert int(count[0]) == int(oc[0]) == k
+    assert np.allclose(score.cpu().numpy(), osc, atol=2 * TOL_F32)
+    assert sorted(idx[0].tolist()) == sorted(w.planted[0]["pos"].tolist())
+
+
+@pytest.mark.parametrize("name,over", [
+    ("c2", dict(R=2, T=300, d=256)),                    # V = 151936: ragged last V-tile
+    ("c3", dict(R=1, T=520, d=256)),
+    ("c4", dict(R=3, T=700, d=128, V=20000)),           # agent observation spans
+    ("c5", dict(R=1, T=400, d=256)),                     # heavy-tailed, V = 152064
+])
+def test_bf16_reduced_configs_all_rows(hdl, name, over):
+    w = workloads.make_workload(name, **over)
+    _check_all_rows(hdl, w, TOL_BF16)
+
+
+@pytest.mark.parametrize("n_rows,d,V", [
+    (1, 64, 256),          # a single row, a single exact tile
+    (257, 64, 257),        # ragged rows and one vocab row past a tile
+    (511, 8, 1000),        # K tail: d smaller than one K-slice
+    (300, 72, 4133),       # K tail after a full slice, ragged vocab
+    (64, 136, 513),
+    (1000, 2056, 2048),    # long K with a tail
+])
+def test_bf16_shape_edges(hdl, n_rows, d, V):
+    g = torch.Generator().manual_seed(n_rows * 7 + d * 13 + V)
+    W = (torch.randn(V, d, generator=g) * 0.05).to(torch.bfloat16)
+    H = torch.randn(n_rows, d, generator=g).to(torch.bfloat16)
+    y = torch.randint(0, V, (n_rows,), generator=g, dtype=torch.int32)
+    lp, lse = run_logprobs(hdl, H, W, y, None)
+    want, want_lse = oracle_rows(H, W, y, np.arange(n_rows))
+    assert np.abs(lp - want).max() <= TOL_BF16
+    assert np.abs(lse - want_lse).max() <= TOL_BF16
+
+
+@pytest.mark.parametrize("n_rows,d,V", [(300, 40, 777), (513, 256, 4096), (70, 24, 300)])
+def test_f32_shape_edges(hdl, n_rows, d, V):
+    g = torch.Generator().manual_seed(n_rows + d + V)
+    W = torch.randn(V, d, generator=g) * 0.05
+    H = torch.randn(n_rows, d, generator=g)
+    y = torch.randint(0, V, (n_rows,), generator=g, dtype=torch.int32)
+    lp, _ = run_logprobs(hdl, H, W, y, None)
+    want, _ = oracle_rows(H, W, y, np.arange(n_rows))
+    assert np.abs(lp - want).max() <= TOL_F32
+
+
+def test_masks_empty_single_and_sparse(hdl):
+    g = torch.Generator().manual_seed(5)
+    n, d, V = 900, 64, 3000
+    W = (torch.randn(V, d, generator=g) * 0.05).to(torch.bfloat16)
+    H = torch.randn(n, d, generator=g).to(torch.bfloat16)
+    y = torch.randint(0, V, (n,), generator=g, dtype=torch.int32)
+    # nothing eligible: every output is 0, no kernel work
+    lp, lse = run_logprobs(hdl, H, W, y, torch.zeros(n, dtype=torch.uint8))
+    assert np.all(lp == 0.0) and np.all(lse == 0.0)
+    # one eligible row
+    m = torch.zeros(n, dtype=torch.uint8); m[637] = 1
+    lp, _ = run_logprobs(hdl, H, W, y, m)
+    want, _ = oracle_rows(H, W, y, [637])
+    assert abs(lp[637] - want[0]) <= TOL_BF16 and np.count_nonzero(lp) == 1
+    # sparse random mask: compacted rows straddle several tiles
+    m = (torch.rand(n, generator=g) < 0.3).to(torch.uint8)
+    lp, _ = run_logprobs(hdl, H, W, y, m)
+    rows = np.nonzero(m.numpy())[0]
+    want, _ = oracle_rows(H, W, y, rows)
+    assert np.abs(lp[rows] - want).max() <= TOL_BF16
+    assert np.all(lp[m.numpy() == 0] == 0.0)
+
+
+def test_out_of_range_tokens_give_nan(hdl):
+    g = torch.Generator().manual_seed(6)
+    n, d, V = 40, 64, 500
+    W = (torch.randn(V, d, generator=g) * 0.05).to(torch.bfloat16)
+    H = torch.randn(n, d, generator=g).to(torch.bfloat16)
+    y = torch.randint(0, V, (n,), generator=g, dtype=torch.int32)
+    y[3] = -1; y[17] = V; y[30] = 2 ** 31 - 1
+    lp, _ = run_logprobs(hdl, H, W, y, None)
+    bad = [3, 17, 30]
+    assert np.all(np.isnan(lp[bad]))
+    good = [i for i in range(n) if i not in bad]
+    want, _ = oracle_rows(H, W, y, good)
+    assert np.abs(lp[good] - want).max() <= TOL_BF16
+
+
+def test_probabilities_sum_to_one_by_sweep(hdl):
+    # one hidden row repeated V times, tokens 0..V-1: sum_v p_v must be 1
+    w = workloads.make_workload("tiny")
+    V = w.cfg.V
+    h = w.hidden[1, 0, 37].reshape(1, -1).repeat(V, 1)
+    lp, _ = run_logprobs(hdl, h, w.W, torch.arange(V, dtype=torch.int32), None)
+    assert abs(math.fsum(np.exp(lp.astype(np.float64))) - 1.0) < 1e-4
+
+
+def test_identical_contexts_give_bitwise_zero_delta(hdl):
+    w = workloads.make_workload("c2", R=2, T=300, d=256, V=5000)
+    c = w.cfg
+    h0 = w.hidden[0].reshape(c.R * c.T, c.d)
+    hidden = torch.cat([h0, h0])           # hindsight := original
+    tokens = w.rows_tokens()
+    lp, _ = run_logprobs(hdl, hidden, w.W, tokens, w.rows_mask())
+    n = c.R * c.T
+    assert np.array_equal(lp[:n].view(np.uint32), lp[n:].view(np.uint32))
+    lpt = torch.from_numpy(lp).cuda()
+    idx, score, count, delta = hdl.select_branch_points(lpt[:n].view(c.R, c.T), lpt[n:].view(c.R, c.T),
+                                                        w.mask.cuda(), c.k, want_delta=True)
+    torch.cuda.synchronize()
+    assert torch.all(delta == 0) and torch.all(score == 0)
+    # all-zero scores: the first k eligible positions, in order
+    first = [np.nonzero(w.mask[r].numpy())[0][:c.k].tolist() for r in range(c.R)]
+    assert idx.cpu().numpy().tolist() == first
+
+
+def test_duplicate_rows_bitwise_equal_across_tiles(hdl):
+    g = torch.Generator().manual_seed(8)
+    n, d, V = 1100, 128, 4100
+    W = (torch.randn(V, d, generator=g) * 0.05).to(torch.bfloat16)
+    H = torch.randn(n, d, generator=g).to(torch.bfloat16)
+    y = torch.randint(0, V, (n,), generator=g, dtype=torch.int32)
+    for src, dst in [(3, 300), (10, 1099), (511, 512), (0, 767)]:
+        H[dst] = H[src]; y[dst] = y[src]
+    lp, lse = run_logprobs(hdl, H, W, y, None)
+    for src, dst in [(3, 300), (10, 1099), (511, 512), (0, 767)]:
+        assert lp[src].view(np.uint32) == lp[dst].view(np.uint32)
+        assert lse[src].view(np.uint32) == lse[dst].view(np.uint32)
+
+
+def test_run_to_run_determinism(hdl):
+    w = workloads.make_workload("c4", R=2, T=1200, d=128, V=9000)
+    hidden, W, tokens, mask = flat_inputs(w)
+    a, _ = run_logprobs(hdl, hidden, W, tokens, mask)
+    b, _ = run_logprobs(hdl, hidden, W, tokens, mask)
+    assert np.array_equal(a.view(np.uint32), b.view(np.uint32))
+
+
+def test_vocab_permutation_invariance(hdl):
+    g = torch.Generator().manual_seed(9)
+    n, d, V = 300, 64, 3001
+    W = (torch.randn(V, d, generator=g) * 0.05).to(torch.bfloat16)
+    H = torch.randn(n, d, generator=g).to(torch.bfloat16)
+    y = torch.randint(0, V, (n,), generator=g, dtype=torch.int32)
+    perm = torch.randperm(V, generator=g)
+    inv = torch.argsort(perm)
+    a, _ = run_logprobs(hdl, H, W, y, None)
+    b, _ = run_logprobs(hdl, H, W[perm].contiguous(), inv[y.long()].to(torch.int32), None)
+    assert np.abs(a - b).max() <= 1e-5
+
+
+# ------------------------------------------------------------ selection alone
+@pytest.mark.parametrize("R,T,k,nan_rows", [
+    (1, 1, 1, 0), (3, 7, 4, 0), (2, 1023, 8, 1), (2, 1024, 32, 0), (4, 1025, 16, 2),
+    (2, 32768, 32, 3), (1, 40000, 1024, 0), (32, 8192, 8, 1), (5, 300, 1024, 0),
+])
+def test_select_bit_exact_vs_oracle(hdl, R, T, k, nan_rows):
+    lo, lh, mask = workloads.make_logp_pair(R, T, seed=R * 1000 + T + k, nan_rows=nan_rows)
+    idx, score, count, delta = hdl.select_branch_points(torch.from_numpy(lo).cuda(), torch.from_numpy(lh).cuda(),
+                                                        torch.from_numpy(mask).cuda(), k, want_delta=True)
+    torch.cuda.synchronize()
+    oi, osc, oc = O.select_branch_points(lo, lh, mask, k, precision="f32")
+    sd, _, _ = O.divergence(lo, lh, mask, precision="f32")
+    assert np.array_equal(count.cpu().numpy(), oc)
+    assert np.array_equal(idx.cpu().numpy(), oi)
+    assert np.array_equal(score.cpu().numpy().view(np.uint32), osc.astype(np.float32).view(np.uint32))
+    assert np.array_equal(delta.cpu().numpy().view(np.uint32), sd.view(np.uint32))
+
+
+def test_select_ties_at_boundary_take_lower_index(hdl):
+    T = 5000
+    lo = np.full((2, T), -2.0, np.float32)
+    lh = lo.copy()
+    lh[:, [4000, 17, 2500, 3, 4999]] = -1.0        # five exact ties at s = 1
+    lh[:, 1000] = 0.0                                # one clear winner, s = 2
+    mask = np.ones((2, T), np.uint8)
+    mask[1, 3] = 0
+    idx, score, count, _ = hdl.select_branch_points(torch.from_numpy(lo).cuda(), torch.from_numpy(lh).cuda(),
+                                                    torch.from_numpy(mask).cuda(), 4)
+    torch.cuda.synchronize()
+    assert idx[0].tolist() == [1000, 3, 17, 2500]
+    assert idx[1].tolist() == [1000, 17, 2500, 4000]
+    assert score[0].tolist() == [2.0, 1.0, 1.0, 1.0]
+
+
+def test_select_fewer_candidates_than_k(hdl):
+    lo = np.array([[-1.0, -2.0, -3.0, -4.0]], np.float32)
+    lh = np.array([[-1.5, np.nan, -1.0, -9.0]], np.float32)
+    mask = np.array([[1, 1, 1, 0]], np.uint8)
+    idx, score, count, _ = hdl.select_branch_points(torch.from_numpy(lo).cuda(), torch.from_numpy(lh).cuda(),
+                                                    torch.from_numpy(mask).cuda(), 6)
+    torch.cuda.synchronize()
+    assert int(count[0]) == 2
+    assert idx[0].tolist() == [2, 0, -1, -1, -1, -1]
+    assert score[0].tolist() == [2.0, 0.5, 0.0, 0.0, 0.0, 0.0]
+
+
+def test_select_without_mask(hdl):
+    lo, lh, _ = workloads.make_logp_pair(3, 2000, seed=3)
+    idx, _, count, _ = hdl.select_branch_points(torch.from_numpy(lo).cuda(), torch.from_numpy(lh).cuda(), None, 10)
+    torch.cuda.synchronize()
+    oi, _, oc = O.select_branch_points(lo, lh, None, 10, precision="f32")
+    assert np.array_equal(idx.cpu().numpy(), oi) and np.array_equal(count.cpu().numpy(), oc)
+
+
+def test_boundary_errors(hdl):
+    dev = "cuda"
+    H = torch.zeros(4, 12, dtype=torch.bfloat16, device=dev)     # d = 12: not a multiple of 8
+    W = torch.zeros(10, 12, dtype=torch.bfloat16, device=dev)
+    y = torch.zeros(4, dtype=torch.int32, device=dev)
+    with pytest.raises(hdl.HdlError) as e:
+        hdl.token_logprobs(H, W, y)
+    assert e.value.status == -2
+    lo = torch.zeros(2, 5, device=dev)
+    with pytest.raises(hdl.HdlError) as e:
+        hdl.select_branch_points(lo, lo, None, 2000)
+    assert e.value.status == -2
+    H = torch.zeros(4, 16, dtype=torch.bfloat16, device=dev)
+    W = torch.zeros(10, 16, dtype=torch.bfloat16, device=dev)
+    small = torch.empty(16, dtype=torch.uint8, device=dev)
+    with pytest.raises(hdl.HdlError) as e:
+        hdl.token_logprobs(H, W, y, workspace=small)
+    assert e.value.status == -3
