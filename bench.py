@@ -35,6 +35,28 @@ def log(msg: str) -> None:
     print(f"[bench] {msg}", file=sys.stderr, flush=True)
 
 
+def kernel_source_sha() -> str:
+    import hashlib
+    path = os.path.join(ROOT, "paper_2609_36864_amd", "csrc", "lmhead_logprob.hip")
+    with open(path, "rb") as f:
+        return hashlib.sha256(f.read()).hexdigest()
+
+
+def measured_traffic(workload: str):
+    """HBM bytes per launch of the fused kernel, from the committed rocprofv3
+    FETCH_SIZE / WRITE_SIZE summary, if it was taken on the current kernel
+    source; otherwise None."""
+    path = os.path.join(ROOT, "profiles", f"lmhead_logprob_{workload}_traffic.json")
+    try:
+        with open(path) as f:
+            rec = json.load(f)
+    except (OSError, ValueError):
+        return None
+    if rec.get("kernel_source_sha256") != kernel_source_sha():
+        return None
+    return rec.get("hbm_bytes_per_launch")
+
+
 def cpu_baseline(w, budget_s: float = 15.0, max_rows: int = 4096):
     """Time the float64 oracle on a seeded sample of eligible rows (both
     contexts) on the host cores; return oracle scored tokens/s."""
@@ -80,6 +102,9 @@ def main() -> int:
     ap.add_argument("--workload", default="c2", help="tiny | c2 | c3 | c4 | c5 (default c2)")
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--cpu-budget", type=float, default=15.0)
+    ap.add_argument("--copy-probe-mb", type=int, default=0,
+                    help="after timing, copy this many MiB device-to-device once (a known-size "
+                         "kernel that calibrates rocprofv3 FETCH_SIZE / WRITE_SIZE)")
     args = ap.parse_args()
 
     if args.gpus != 1 or int(os.environ.get("WORLD_SIZE", "1")) != 1:
@@ -178,6 +203,16 @@ def main() -> int:
                      "kernel": "lmhead_logprob_kernel", "kernel_ms": kern_avg_ms,
                      "flops_per_launch": flops},
     }
+    if args.copy_probe_mb > 0:
+        src = torch.empty(args.copy_probe_mb << 20, dtype=torch.uint8, device=dev).fill_(1)
+        dst = torch.empty_like(src)
+        torch.cuda.synchronize()
+        dst.copy_(src)
+        torch.cuda.synchronize()
+        log(f"copy probe: {args.copy_probe_mb} MiB device-to-device")
+    traffic = measured_traffic(args.workload)
+    if traffic is not None:
+        result["roofline"]["traffic"] = traffic
     if not args.no_cpu_baseline:
         log("timing the float64 oracle on a bounded sample")
         result["cpu_baseline"] = cpu_baseline(w, budget_s=args.cpu_budget)

@@ -20,10 +20,15 @@
 // a V-tile is entirely lane-local, and lanes and waves are merged only once
 // per work item.
 //
-// Operands stream through LDS in K-slices of 128 bytes per row (64 bf16 or 32
-// fp32), double-buffered, with an XOR swizzle of the 16-byte chunks so that
-// the 32-row fragment reads are bank-conflict free.  Global loads for slice
-// i+1 are in flight while slice i is multiplied.
+// Operands stream through LDS in K-slices of 64 bytes per row (32 bf16 or 16
+// fp32; HDL_LDS_CHUNKS=8 selects 128-byte slices) with a ring of
+// HDL_LDS_STAGES (default 4) stages: later slices are in flight (global ->
+// LDS DMA, no VGPR staging) while slice i is multiplied.  16-byte chunks are XOR
+// swizzled so that the 32-row fragment reads are bank-conflict free.  The
+// DMA is issued from inline assembly and waited for with explicit vmcnt
+// counts: the compiler cannot see that a DMA into one stage does not alias
+// the reads of another, and would otherwise wait for every outstanding DMA
+// before each LDS read.
 //
 // Both operands are contiguous in K.  MFMA lane l takes row (l mod 32) and a
 // 16-byte K fragment chosen by (l div 32); A and B fragments use the same K
@@ -40,20 +45,74 @@ typedef __bf16 bf16x8_t __attribute__((ext_vector_type(8)));
 typedef float f32x16_t __attribute__((ext_vector_type(16)));
 
 constexpr int kThreads = 256;
-constexpr int kChunks = 8;                          // 16-byte chunks per LDS row
-constexpr int kRowsPerPass = kThreads / kChunks;    // 32 rows per cooperative load
-constexpr int kLoads = kTileV / kRowsPerPass;       // 8 loads per operand per slice
-constexpr int kTileElems = kTileV * kChunks;        // uint4 slots per operand tile
+#ifndef HDL_LDS_CHUNKS
+#define HDL_LDS_CHUNKS 4
+#endif
+#ifndef HDL_LDS_STAGES
+#define HDL_LDS_STAGES 4
+#endif
+constexpr int kChunks = HDL_LDS_CHUNKS;             // 16-byte chunks per LDS row per stage
+constexpr int kStages = HDL_LDS_STAGES;             // LDS ring depth (K-slices)
+constexpr int kSlots = kTileV * kChunks;            // uint4 slots per operand per stage
+constexpr int kBlockRows = 64 / kChunks;            // rows per 1 KB DMA block
+constexpr int kBlocksPerWave = kTileV / kBlockRows / 4;   // DMA blocks per operand per wave
+constexpr int kDmaPerSlice = 2 * kBlocksPerWave;    // DMA instructions per lane per slice
+constexpr int kSub = kChunks / 2;                   // MFMA sub-steps per slice
 constexpr float kLog2e = 1.4426950408889634f;
 constexpr float kNegInf = -__builtin_inff();
 
 static_assert(kTileV == kTileN, "square workgroup tile assumed");
+static_assert(kChunks == 4 || kChunks == 8, "64- or 128-byte K-slices");
+static_assert(kStages * 2 * kSlots * 16 <= 160 * 1024, "LDS ring exceeds 160 KB");
+static_assert(kDmaPerSlice * (kStages - 1) <= 63, "vmcnt range");
 
+// XOR pattern of a row: consecutive rows of one 32-row fragment read land in
+// distinct 16-byte bank groups.
+__device__ __forceinline__ int row_xor(int row) {
+  return kChunks == 8 ? (row & 7) : ((row >> 1) & 3);
+}
+
+// Slot of (row, logical 16-byte chunk) in a [rows][kChunks] LDS tile.
 __device__ __forceinline__ int swz(int row, int chunk) {
-  return row * kChunks + (chunk ^ (row & 7));
+  return row * kChunks + (chunk ^ row_xor(row));
 }
 
 __device__ __forceinline__ float fast_exp2(float x) { return __builtin_amdgcn_exp2f(x); }
+
+// 16 bytes per lane from global memory straight into LDS at lds_base + 16*lane.
+// M0 carries the LDS base; it is saved and restored around the DMA so the
+// compiler's own use of M0 is unaffected.
+__device__ __forceinline__ void dma16(const char* gptr, uint32_t lds_base) {
+  uint32_t saved;
+  asm volatile(
+      "s_mov_b32 %0, m0\n\t"
+      "s_mov_b32 m0, %1\n\t"
+      "s_nop 0\n\t"
+      "global_load_lds_dwordx4 %2, off\n\t"
+      "s_mov_b32 m0, %0"
+      : "=&s"(saved)
+      : "s"(lds_base), "v"(gptr)
+      : "memory");
+}
+
+// Wait until at most `slices` K-slices of this lane's DMA are outstanding.
+template <int N>
+__device__ __forceinline__ void wait_vmcnt() {
+  asm volatile("s_waitcnt vmcnt(%0)" ::"n"(N) : "memory");
+}
+__device__ __forceinline__ void wait_dma(int slices) {
+  if (kStages > 3 && slices >= 3) wait_vmcnt<(kStages > 3 ? 3 : 0) * kDmaPerSlice>();
+  else if (kStages > 2 && slices >= 2) wait_vmcnt<(kStages > 2 ? 2 : 0) * kDmaPerSlice>();
+  else if (slices >= 1) wait_vmcnt<kDmaPerSlice>();
+  else wait_vmcnt<0>();
+}
+
+// Workgroup barrier without the memory fence __syncthreads() implies (the
+// fence would wait for every in-flight DMA).  LDS reads issued before it
+// are complete: callers wait lgkmcnt(0) first.
+__device__ __forceinline__ void raw_barrier() {
+  asm volatile("s_waitcnt lgkmcnt(0)\n\ts_barrier" ::: "memory");
+}
 
 // One MFMA step over a pair of 16-byte fragments (same K positions in A, B).
 template <bool BF16> struct Mma;
@@ -99,7 +158,7 @@ __global__ __launch_bounds__(kThreads, 1) void lmhead_logprob_kernel(LmheadArgs 
   constexpr int kEsz = BF16 ? 2 : 4;
   constexpr int kSliceK = M::kElemsPer16B * kChunks;   // K elements per slice
 
-  __shared__ uint4 lds[2][2][kTileElems];   // [stage][0 = W, 1 = hidden]
+  __shared__ uint4 lds[kStages][2][kSlots];   // [stage][0 = W, 1 = hidden] = 128 KB
 
   const int tid = threadIdx.x;
   const int lane = tid & 63;
@@ -157,63 +216,82 @@ __global__ __launch_bounds__(kThreads, 1) void lmhead_logprob_kernel(LmheadArgs 
       for (int q = 0; q < 16; ++q) acc[bm][bn][q] = 0.f;
 
   // ---- direct global -> LDS loads -----------------------------------------
-  // A K-slice of one operand tile is 32 blocks of 8 rows x 128 bytes.  Wave
-  // w fetches blocks 8w .. 8w+7; within a block lane l lands in LDS slot l,
-  // i.e. row l/8 and physical chunk l%8, so it fetches logical chunk
-  // (l%8) ^ (l/8) of that row (the inverse of the read swizzle).
-  const int lrow = lane >> 3;
-  const int lchunk = (lane & 7) ^ lrow;
+  // A K-slice of one operand tile is made of 1 KB blocks of kBlockRows rows.
+  // Wave w fetches blocks w*kBlocksPerWave ..; within a block lane l lands in
+  // LDS slot l, i.e. row l/kChunks and physical chunk l%kChunks, so it
+  // fetches the logical chunk that the read swizzle maps there.
+  const int lrow = lane / kChunks;
+  const int lrow_xor = row_xor(lrow);   // blocks start at multiples of 8 rows
+  const int lchunk = (lane % kChunks) ^ lrow_xor;
   const bool k_tail = (d % kSliceK) != 0;
-  const char* hp[kLoads];
+  const char* hp[kBlocksPerWave];
 #pragma unroll
-  for (int i = 0; i < kLoads; ++i) {
-    int64_t e = rt * kTileN + wave * 64 + i * 8 + lrow;
+  for (int i = 0; i < kBlocksPerWave; ++i) {
+    int64_t e = rt * kTileN + wave * 64 + i * kBlockRows + lrow;
     e = e < n_s ? e : n_s - 1;
     hp[i] = hbase + static_cast<int64_t>(p.rows[e]) * d * kEsz;
   }
-  const char* wp[kLoads];
+  const char* wp[kBlocksPerWave];
   auto set_w = [&](int64_t vt) {
 #pragma unroll
-    for (int i = 0; i < kLoads; ++i) {
-      int64_t v = vt * kTileV + wave * 64 + i * 8 + lrow;
+    for (int i = 0; i < kBlocksPerWave; ++i) {
+      int64_t v = vt * kTileV + wave * 64 + i * kBlockRows + lrow;
       v = v < V ? v : V - 1;
       wp[i] = wbase + v * d * kEsz;
     }
   };
-  auto issue = [&](int it, int stage) {
-    const int kt = it % nk;
-    if (kt == 0) set_w(vt0 + it / nk);
-    int64_t koff = (static_cast<int64_t>(kt) * kSliceK + lchunk * M::kElemsPer16B);
-    if (k_tail && koff >= d) koff = 0;   // in-bounds dummy; zeroed after arrival
-    koff *= kEsz;
-#pragma unroll
-    for (int i = 0; i < kLoads; ++i)
-      __builtin_amdgcn_global_load_lds(
-          (const __attribute__((address_space(1))) void*)(wp[i] + koff),
-          (__attribute__((address_space(3))) void*)(&lds[stage][0][(wave * kLoads + i) * 64]),
-          16, 0, 0);
-#pragma unroll
-    for (int i = 0; i < kLoads; ++i)
-      __builtin_amdgcn_global_load_lds(
-          (const __attribute__((address_space(1))) void*)(hp[i] + koff),
-          (__attribute__((address_space(3))) void*)(&lds[stage][1][(wave * kLoads + i) * 64]),
-          16, 0, 0);
+  const uint32_t lds_base = static_cast<uint32_t>(
+      reinterpret_cast<size_t>((__attribute__((address_space(3))) uint4*)(&lds[0][0][0])));
+  auto lds_addr = [&](int stage, int op, int block) -> uint32_t {
+    return __builtin_amdgcn_readfirstlane(
+        lds_base + static_cast<uint32_t>(((stage * 2 + op) * kSlots + block * 64) * 16));
   };
-  // Wait for this thread's LDS-bound loads; on the last K-slice of a row
-  // whose length is not a multiple of the slice, clear the chunks past d.
-  auto arrive = [&](int it, int stage) {
-    asm volatile("s_waitcnt vmcnt(0)" ::: "memory");
-    if (k_tail && (it % nk) == nk - 1) {
-      for (int sidx = tid; sidx < kTileElems; sidx += kThreads) {
-        const int row = sidx >> 3;
-        const int chunk = (sidx & 7) ^ (row & 7);
-        if (static_cast<int64_t>(it % nk) * kSliceK + chunk * M::kElemsPer16B >= d) {
-          lds[stage][0][sidx] = make_uint4(0, 0, 0, 0);
-          lds[stage][1][sidx] = make_uint4(0, 0, 0, 0);
-        }
+  // DMA j (0 .. kDmaPerSlice-1) of K-slice `slice`; j < kBlocksPerWave are W
+  // blocks, the rest hidden-state blocks.  prep_issue() must run first.
+  int64_t issue_koff = 0;
+  int issue_stage = 0;
+  auto prep_issue = [&](int slice) {
+    issue_stage = slice % kStages;
+    const int kt = slice % nk;
+    if (kt == 0) set_w(vt0 + slice / nk);
+    int64_t koff = static_cast<int64_t>(kt) * kSliceK + lchunk * M::kElemsPer16B;
+    if (k_tail && koff >= d) koff = 0;   // in-bounds dummy; zeroed after arrival
+    issue_koff = koff * kEsz;
+  };
+  auto issue_one = [&](int j) {
+    if (j < kBlocksPerWave)
+      dma16(wp[j] + issue_koff, lds_addr(issue_stage, 0, wave * kBlocksPerWave + j));
+    else
+      dma16(hp[j - kBlocksPerWave] + issue_koff,
+            lds_addr(issue_stage, 1, wave * kBlocksPerWave + j - kBlocksPerWave));
+  };
+  auto issue = [&](int slice) {
+    prep_issue(slice);
+#pragma unroll
+    for (int j = 0; j < kDmaPerSlice; ++j) issue_one(j);
+  };
+
+  // On the last K-slice of a row whose length is not a multiple of the
+  // slice, clear the chunks past d (between two barriers: the DMA of every
+  // wave must have landed before, and no wave may read before it is done).
+  auto clear_k_tail = [&](int slice) {
+    const int stage = slice % kStages;
+    const int kt = slice % nk;
+    for (int sidx = tid; sidx < kSlots; sidx += kThreads) {
+      const int row = sidx / kChunks;
+      const int chunk = (sidx % kChunks) ^ row_xor(row);
+      if (static_cast<int64_t>(kt) * kSliceK + chunk * M::kElemsPer16B >= d) {
+        lds[stage][0][sidx] = make_uint4(0, 0, 0, 0);
+        lds[stage][1][sidx] = make_uint4(0, 0, 0, 0);
       }
     }
-    __syncthreads();
+  };
+  auto load_frags = [&](int slice, int kk, uint4 (&fa)[4], uint4 (&fb)[4]) {
+    const int stage = slice % kStages;
+#pragma unroll
+    for (int bm = 0; bm < 4; ++bm) fa[bm] = lds[stage][0][swz(wm * 128 + bm * 32 + col, kk * 2 + half)];
+#pragma unroll
+    for (int bn = 0; bn < 4; ++bn) fb[bn] = lds[stage][1][swz(wn * 128 + bn * 32 + col, kk * 2 + half)];
   };
 
   // Online max / sum-of-exp update of one V-tile, then capture of the
@@ -274,34 +352,47 @@ __global__ __launch_bounds__(kThreads, 1) void lmhead_logprob_kernel(LmheadArgs 
         for (int q = 0; q < 16; ++q) acc[bm][bn][q] = 0.f;
   };
 
-  issue(0, 0);
-  arrive(0, 0);
+  // ---- pipelined main loop over (V-tile, K-slice) ------------------------
+  const int n_pre = n_iter < kStages ? n_iter : kStages;
+  for (int sl = 0; sl < n_pre; ++sl) issue(sl);
+  wait_dma(n_pre - 1);
+  raw_barrier();
+  if (k_tail && nk == 1) { clear_k_tail(0); raw_barrier(); }
 
-  int it = 0;
+  // 16 MFMAs of one sub-step.
+  auto mfma_step = [&](const uint4 (&a)[4], const uint4 (&b)[4]) {
+#pragma unroll
+    for (int j = 0; j < 16; ++j) M::run(a[j >> 2], b[j & 3], acc[j >> 2][j & 3]);
+  };
+
+  uint4 fa[2][4], fb[2][4];
+  int it = 0;   // global slice counter
   for (int64_t vt = vt0; vt < vt1; ++vt) {
+    load_frags(it, 0, fa[0], fb[0]);
     for (int kt = 0; kt < nk; ++kt, ++it) {
-      const int stage = it & 1;
-      if (it + 1 < n_iter) issue(it + 1, stage ^ 1);
+      const bool last_k = kt == nk - 1;
 #pragma unroll
-      for (int kk = 0; kk < 4; ++kk) {
-        uint4 af[4], bf[4];
-#pragma unroll
-        for (int bm = 0; bm < 4; ++bm)
-          af[bm] = lds[stage][0][swz(wm * 128 + bm * 32 + col, kk * 2 + half)];
-#pragma unroll
-        for (int bn = 0; bn < 4; ++bn)
-          bf[bn] = lds[stage][1][swz(wn * 128 + bn * 32 + col, kk * 2 + half)];
-#pragma unroll
-        for (int bm = 0; bm < 4; ++bm)
-#pragma unroll
-          for (int bn = 0; bn < 4; ++bn) M::run(af[bm], bf[bn], acc[bm][bn]);
+      for (int kk = 0; kk < kSub; ++kk) {
+        const int cur = kk & 1;
+        if (kk + 1 < kSub) {
+          load_frags(it, kk + 1, fa[cur ^ 1], fb[cur ^ 1]);
+        } else if (it + 1 < n_iter) {
+          // every read of slice `it` is issued: wait for slice it+1, then
+          // recycle this slice's stage for slice it+kStages
+          const int after = n_iter - 2 - it;
+          wait_dma(after < kStages - 2 ? after : kStages - 2);
+          raw_barrier();
+          if (k_tail && ((it + 1) % nk) == nk - 1) { clear_k_tail(it + 1); raw_barrier(); }
+          if (it + kStages < n_iter) issue(it + kStages);
+          if (!last_k) load_frags(it + 1, 0, fa[cur ^ 1], fb[cur ^ 1]);
+        }
+        mfma_step(fa[cur], fb[cur]);
       }
-      if (it + 1 < n_iter) arrive(it + 1, stage ^ 1);
-      else __syncthreads();
     }
     if ((vt + 1) * kTileV <= V) epilogue(vt, std::false_type{});
     else epilogue(vt, std::true_type{});
   }
+  __syncthreads();
 
   // ---- merge the two lane halves, then the two vocabulary waves -----------
 #pragma unroll
