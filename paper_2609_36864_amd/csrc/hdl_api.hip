@@ -46,8 +46,15 @@ Profiler g_prof;
 
 namespace hdl {
 
-LmheadPlan make_plan(int64_t n_rows, int64_t vocab) {
+int64_t rows_per_launch(int64_t d, int esz) {
+  const int64_t row_bytes = d * esz;
+  return ((int64_t{1} << 32) / row_bytes) / kTileN * kTileN;
+}
+
+LmheadPlan make_plan(int64_t n_rows_total, int64_t vocab, int64_t d, int esz) {
   LmheadPlan p{};
+  p.rows_per_launch = rows_per_launch(d, esz);
+  const int64_t n_rows = n_rows_total < p.rows_per_launch ? n_rows_total : p.rows_per_launch;
   p.n_rows = n_rows;
   p.n_vt = (vocab + kTileV - 1) / kTileV;
   p.n_rt_max = (n_rows + kTileN - 1) / kTileN;
@@ -83,7 +90,9 @@ extern "C" {
 size_t hdl_token_logprobs_workspace_size(int64_t n_rows, int64_t d, int64_t vocab, int dtype) {
   if (n_rows <= 0 || d <= 0 || vocab <= 0 || n_rows > INT32_MAX || vocab > INT32_MAX) return 0;
   if (dtype != HDL_F32 && dtype != HDL_BF16) return 0;
-  return hdl::make_plan(n_rows, vocab).bytes;
+  const int esz = dtype == HDL_BF16 ? 2 : 4;
+  if (hdl::rows_per_launch(d, esz) < hdl::kTileN) return 0;
+  return hdl::make_plan(n_rows, vocab, d, esz).bytes;
 }
 
 int hdl_token_logprobs(const void* hidden, const void* w_vocab, const int32_t* tokens,
@@ -104,7 +113,10 @@ int hdl_token_logprobs(const void* hidden, const void* w_vocab, const int32_t* t
     return fail(HDL_ERR_UNSUPPORTED, "hdl_token_logprobs: d=%lld is not a multiple of 8", static_cast<long long>(d));
   if (!aligned(hidden, 16) || !aligned(w_vocab, 16))
     return fail(HDL_ERR_INVALID_ARG, "hdl_token_logprobs: hidden and w_vocab must be 16-byte aligned");
-  const hdl::LmheadPlan plan = hdl::make_plan(n_rows, vocab);
+  const int esz = dtype == HDL_BF16 ? 2 : 4;
+  if (hdl::rows_per_launch(d, esz) < hdl::kTileN)
+    return fail(HDL_ERR_UNSUPPORTED, "hdl_token_logprobs: hidden rows larger than 16 MiB");
+  const hdl::LmheadPlan plan = hdl::make_plan(n_rows, vocab, d, esz);
   if (!workspace || workspace_bytes < plan.bytes)
     return fail(HDL_ERR_WORKSPACE, "hdl_token_logprobs: workspace of %zu bytes needed, %zu given",
                 plan.bytes, workspace ? workspace_bytes : static_cast<size_t>(0));
@@ -118,52 +130,61 @@ int hdl_token_logprobs(const void* hidden, const void* w_vocab, const int32_t* t
   int32_t* rows = reinterpret_cast<int32_t*>(ws + plan.off_rows);
   int32_t* n_scored = reinterpret_cast<int32_t*>(ws + plan.off_count);
   float* part = reinterpret_cast<float*>(ws + plan.off_part);
-  const size_t plane = static_cast<size_t>(plan.n_ch) * static_cast<size_t>(n_rows);
+  const size_t plane = static_cast<size_t>(plan.n_ch) * static_cast<size_t>(plan.n_rows);
+  const int64_t row_bytes = d * esz;
 
-  hipError_t e = hdl::launch_compact(mask, n_rows, rows, n_scored, logp, lse_out, s);
-  if (e != hipSuccess) return hip_fail(e, "compaction launch");
+  // Launches of at most plan.rows_per_launch rows each (one launch for every
+  // configuration up to 4 GiB of hidden states).
+  for (int64_t r0 = 0; r0 < n_rows; r0 += plan.rows_per_launch) {
+    const int64_t n = (n_rows - r0) < plan.rows_per_launch ? (n_rows - r0) : plan.rows_per_launch;
+    const hdl::LmheadPlan lp = hdl::make_plan(n, vocab, d, esz);
+    float* logp_c = logp + r0;
+    float* lse_c = lse_out ? lse_out + r0 : nullptr;
+    hipError_t e = hdl::launch_compact(mask ? mask + r0 : nullptr, n, rows, n_scored, logp_c, lse_c, s);
+    if (e != hipSuccess) return hip_fail(e, "compaction launch");
 
-  hdl::LmheadArgs a{};
-  a.hidden = hidden;
-  a.w = w_vocab;
-  a.tokens = tokens;
-  a.rows = rows;
-  a.n_scored = n_scored;
-  a.d = d;
-  a.vocab = vocab;
-  a.n_vt = plan.n_vt;
-  a.tpc = plan.tpc;
-  a.n_ch = plan.n_ch;
-  a.n_grt = plan.n_grt;
-  a.part_stride = n_rows;
-  a.part_m = part;
-  a.part_s = part + plane;
-  a.part_z = part + 2 * plane;
+    hdl::LmheadArgs a{};
+    a.hidden = static_cast<const char*>(hidden) + r0 * row_bytes;
+    a.w = w_vocab;
+    a.tokens = tokens + r0;
+    a.rows = rows;
+    a.n_scored = n_scored;
+    a.d = d;
+    a.vocab = vocab;
+    a.n_vt = lp.n_vt;
+    a.tpc = lp.tpc;
+    a.n_ch = lp.n_ch;
+    a.n_grt = lp.n_grt;
+    a.part_stride = n;
+    a.part_m = part;
+    a.part_s = part + plane;
+    a.part_z = part + 2 * plane;
 
-  std::pair<hipEvent_t, hipEvent_t> ev{nullptr, nullptr};
-  bool timed = false;
-  {
-    std::lock_guard<std::mutex> lk(g_prof.mu);
-    if (g_prof.on) {
-      if (!g_prof.spare.empty()) {
-        ev = g_prof.spare.back();
-        g_prof.spare.pop_back();
-      } else if (hipEventCreate(&ev.first) != hipSuccess || hipEventCreate(&ev.second) != hipSuccess) {
-        return fail(HDL_ERR_HIP, "hdl_token_logprobs: hipEventCreate failed");
+    std::pair<hipEvent_t, hipEvent_t> ev{nullptr, nullptr};
+    bool timed = false;
+    {
+      std::lock_guard<std::mutex> lk(g_prof.mu);
+      if (g_prof.on) {
+        if (!g_prof.spare.empty()) {
+          ev = g_prof.spare.back();
+          g_prof.spare.pop_back();
+        } else if (hipEventCreate(&ev.first) != hipSuccess || hipEventCreate(&ev.second) != hipSuccess) {
+          return fail(HDL_ERR_HIP, "hdl_token_logprobs: hipEventCreate failed");
+        }
+        timed = true;
       }
-      timed = true;
     }
+    if (timed && (e = hipEventRecord(ev.first, s)) != hipSuccess) return hip_fail(e, "hipEventRecord");
+    e = hdl::launch_lmhead(a, lp.grid, dtype == HDL_BF16, s);
+    if (e != hipSuccess) return hip_fail(e, "lm-head kernel launch");
+    if (timed) {
+      if ((e = hipEventRecord(ev.second, s)) != hipSuccess) return hip_fail(e, "hipEventRecord");
+      std::lock_guard<std::mutex> lk(g_prof.mu);
+      g_prof.pending.push_back(ev);
+    }
+    e = hdl::launch_merge(a, n, logp_c, lse_c, s);
+    if (e != hipSuccess) return hip_fail(e, "merge kernel launch");
   }
-  if (timed && (e = hipEventRecord(ev.first, s)) != hipSuccess) return hip_fail(e, "hipEventRecord");
-  e = hdl::launch_lmhead(a, plan.grid, dtype == HDL_BF16, s);
-  if (e != hipSuccess) return hip_fail(e, "lm-head kernel launch");
-  if (timed) {
-    if ((e = hipEventRecord(ev.second, s)) != hipSuccess) return hip_fail(e, "hipEventRecord");
-    std::lock_guard<std::mutex> lk(g_prof.mu);
-    g_prof.pending.push_back(ev);
-  }
-  e = hdl::launch_merge(a, n_rows, logp, lse_out, s);
-  if (e != hipSuccess) return hip_fail(e, "merge kernel launch");
   return HDL_OK;
 }
 

@@ -12,23 +12,26 @@
 // and merge_kernel combines the chunk partials in a fixed order.
 //
 // Work item: 256 vocabulary rows x 256 token rows per V-tile, looping over
-// the V-tiles of one chunk.  Four waves per workgroup, each owning 128 vocab x
-// 128 tokens as a 4x4 grid of 32x32 MFMA blocks (fp32 accumulators).  W is
-// the MFMA "A" operand (vocabulary on the M axis) and the hidden states are
-// the "B" operand (tokens on the N axis), so each lane's accumulators hold one
-// token column and 64 vocabulary rows: the online max / sum-of-exp update of
-// a V-tile is entirely lane-local, and lanes and waves are merged only once
-// per work item.
+// the V-tiles of one chunk.  Eight waves per workgroup (two per SIMD, so one
+// wave's memory and epilogue work overlaps the other's MFMAs), each owning
+// 128 vocab x 64 tokens as a 4x2 grid of 32x32 MFMA blocks with fp32
+// accumulators (HDL_WAVES=4 selects one wave per SIMD with 128 x 128 each).
+// W is the MFMA "A" operand (vocabulary on the M axis) and the hidden states
+// are the "B" operand (tokens on the N axis), so each lane's accumulators
+// hold one token column and 64 vocabulary rows: the online max / sum-of-exp
+// update of a V-tile is entirely lane-local, and lanes and waves are merged
+// only once per work item.
 //
-// Operands stream through LDS in K-slices of 64 bytes per row (32 bf16 or 16
-// fp32; HDL_LDS_CHUNKS=8 selects 128-byte slices) with a ring of
-// HDL_LDS_STAGES (default 4) stages: later slices are in flight (global ->
-// LDS DMA, no VGPR staging) while slice i is multiplied.  16-byte chunks are XOR
-// swizzled so that the 32-row fragment reads are bank-conflict free.  The
-// DMA is issued from inline assembly and waited for with explicit vmcnt
-// counts: the compiler cannot see that a DMA into one stage does not alias
-// the reads of another, and would otherwise wait for every outstanding DMA
-// before each LDS read.
+// Operands stream through LDS in K-slices of 128 bytes per row (64 bf16 or
+// 32 fp32; HDL_LDS_CHUNKS=4 selects 64-byte slices) through a ring of
+// HDL_LDS_STAGES stages (default 2, 128 KB): the next slice is in flight
+// (global -> LDS DMA, no VGPR staging) while slice i is multiplied.  16-byte
+// chunks are XOR swizzled so that the 32-row fragment reads are bank-conflict
+// free.  The DMA is issued from inline assembly (wave-uniform 64-bit base +
+// per-lane 32-bit offset) and waited for with explicit vmcnt counts: the
+// compiler cannot see that a DMA into one stage does not alias the reads of
+// another, and would otherwise wait for every outstanding DMA before each LDS
+// read.
 //
 // Both operands are contiguous in K.  MFMA lane l takes row (l mod 32) and a
 // 16-byte K fragment chosen by (l div 32); A and B fragments use the same K
@@ -44,32 +47,52 @@ namespace {
 typedef __bf16 bf16x8_t __attribute__((ext_vector_type(8)));
 typedef float f32x16_t __attribute__((ext_vector_type(16)));
 
-constexpr int kThreads = 256;
+#ifndef HDL_WAVES
+#define HDL_WAVES 8
+#endif
+constexpr int kWaves = HDL_WAVES;                   // 4: one wave per SIMD; 8: two
+constexpr int kThreads = 64 * kWaves;
+constexpr int kNB = kWaves == 4 ? 4 : 2;            // 32-token MFMA blocks per wave
+constexpr int kWaveN = 32 * kNB;                    // tokens per wave (128 or 64)
 #ifndef HDL_LDS_CHUNKS
-#define HDL_LDS_CHUNKS 4
+#define HDL_LDS_CHUNKS 8
 #endif
 #ifndef HDL_LDS_STAGES
-#define HDL_LDS_STAGES 4
+#define HDL_LDS_STAGES 2
 #endif
 constexpr int kChunks = HDL_LDS_CHUNKS;             // 16-byte chunks per LDS row per stage
 constexpr int kStages = HDL_LDS_STAGES;             // LDS ring depth (K-slices)
 constexpr int kSlots = kTileV * kChunks;            // uint4 slots per operand per stage
 constexpr int kBlockRows = 64 / kChunks;            // rows per 1 KB DMA block
-constexpr int kBlocksPerWave = kTileV / kBlockRows / 4;   // DMA blocks per operand per wave
+constexpr int kBlocksPerWave = kTileV / kBlockRows / kWaves;   // DMA blocks per operand per wave
 constexpr int kDmaPerSlice = 2 * kBlocksPerWave;    // DMA instructions per lane per slice
 constexpr int kSub = kChunks / 2;                   // MFMA sub-steps per slice
 constexpr float kLog2e = 1.4426950408889634f;
 constexpr float kNegInf = -__builtin_inff();
 
 static_assert(kTileV == kTileN, "square workgroup tile assumed");
+static_assert(kWaves == 4 || kWaves == 8, "4 or 8 waves");
 static_assert(kChunks == 4 || kChunks == 8, "64- or 128-byte K-slices");
 static_assert(kStages * 2 * kSlots * 16 <= 160 * 1024, "LDS ring exceeds 160 KB");
 static_assert(kDmaPerSlice * (kStages - 1) <= 63, "vmcnt range");
 
-// XOR pattern of a row: consecutive rows of one 32-row fragment read land in
-// distinct 16-byte bank groups.
+#ifndef HDL_SWZ
+#define HDL_SWZ 1
+#endif
+// XOR pattern of a row: the rows of one 32-row fragment read must land in
+// distinct 16-byte bank groups whether the LDS serves 8 or 16 lanes of a
+// ds_read_b128 per cycle.  With 128-byte rows, (row & 7) ^ ((row >> 3) & 1)
+// does both: 8 consecutive rows get 8 distinct chunks, and rows r and r+8
+// (same bank half when two rows share a 256-byte bank line) differ too.
 __device__ __forceinline__ int row_xor(int row) {
-  return kChunks == 8 ? (row & 7) : ((row >> 1) & 3);
+  if (kChunks == 8) {
+    if (HDL_SWZ == 0) return row & 7;
+    if (HDL_SWZ == 1) return (row & 7) ^ ((row >> 3) & 1);
+    return (row >> 1) & 7;
+  }
+  if (HDL_SWZ == 0) return (row >> 1) & 3;
+  if (HDL_SWZ == 1) return ((row >> 1) & 3) ^ ((row >> 3) & 1);
+  return (row >> 2) & 3;
 }
 
 // Slot of (row, logical 16-byte chunk) in a [rows][kChunks] LDS tile.
@@ -80,18 +103,20 @@ __device__ __forceinline__ int swz(int row, int chunk) {
 __device__ __forceinline__ float fast_exp2(float x) { return __builtin_amdgcn_exp2f(x); }
 
 // 16 bytes per lane from global memory straight into LDS at lds_base + 16*lane.
-// M0 carries the LDS base; it is saved and restored around the DMA so the
-// compiler's own use of M0 is unaffected.
-__device__ __forceinline__ void dma16(const char* gptr, uint32_t lds_base) {
+// The global address is a wave-uniform 64-bit base (SGPRs) plus a per-lane
+// 32-bit byte offset, so issuing a DMA costs no vector ALU work.  M0 carries
+// the LDS base; it is saved and restored around the DMA so the compiler's own
+// use of M0 is unaffected.
+__device__ __forceinline__ void dma16(uint64_t sbase, uint32_t voff, uint32_t lds_base) {
   uint32_t saved;
   asm volatile(
       "s_mov_b32 %0, m0\n\t"
       "s_mov_b32 m0, %1\n\t"
       "s_nop 0\n\t"
-      "global_load_lds_dwordx4 %2, off\n\t"
+      "global_load_lds_dwordx4 %2, %3\n\t"
       "s_mov_b32 m0, %0"
       : "=&s"(saved)
-      : "s"(lds_base), "v"(gptr)
+      : "s"(lds_base), "v"(voff), "s"(sbase)
       : "memory");
 }
 
@@ -162,9 +187,9 @@ __global__ __launch_bounds__(kThreads, 1) void lmhead_logprob_kernel(LmheadArgs 
 
   const int tid = threadIdx.x;
   const int lane = tid & 63;
-  const int wave = tid >> 6;
+  const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);   // wave-uniform
   const int wm = wave & 1;      // which 128 vocabulary rows of the tile
-  const int wn = wave >> 1;     // which 128 token rows of the tile
+  const int wn = wave >> 1;     // which kWaveN token rows of the tile
   const int half = lane >> 5;
   const int col = lane & 31;
 
@@ -195,23 +220,23 @@ __global__ __launch_bounds__(kThreads, 1) void lmhead_logprob_kernel(LmheadArgs 
   const char* __restrict__ hbase = static_cast<const char*>(p.hidden);
 
   // ---- this lane's token columns and their sampled tokens ------------------
-  int tok[4];
+  int tok[kNB];
 #pragma unroll
-  for (int bn = 0; bn < 4; ++bn) {
-    int64_t e = rt * kTileN + wn * 128 + bn * 32 + col;
+  for (int bn = 0; bn < kNB; ++bn) {
+    int64_t e = rt * kTileN + wn * kWaveN + bn * 32 + col;
     e = e < n_s ? e : n_s - 1;
     tok[bn] = p.tokens[p.rows[e]];
   }
 
-  float run_m[4], run_s[4], run_z[4];
+  float run_m[kNB], run_s[kNB], run_z[kNB];
 #pragma unroll
-  for (int bn = 0; bn < 4; ++bn) { run_m[bn] = kNegInf; run_s[bn] = 0.f; run_z[bn] = kNegInf; }
+  for (int bn = 0; bn < kNB; ++bn) { run_m[bn] = kNegInf; run_s[bn] = 0.f; run_z[bn] = kNegInf; }
 
-  f32x16_t acc[4][4];
+  f32x16_t acc[4][kNB];
 #pragma unroll
   for (int bm = 0; bm < 4; ++bm)
 #pragma unroll
-    for (int bn = 0; bn < 4; ++bn)
+    for (int bn = 0; bn < kNB; ++bn)
 #pragma unroll
       for (int q = 0; q < 16; ++q) acc[bm][bn][q] = 0.f;
 
@@ -221,23 +246,31 @@ __global__ __launch_bounds__(kThreads, 1) void lmhead_logprob_kernel(LmheadArgs 
   // LDS slot l, i.e. row l/kChunks and physical chunk l%kChunks, so it
   // fetches the logical chunk that the read swizzle maps there.
   const int lrow = lane / kChunks;
-  const int lrow_xor = row_xor(lrow);   // blocks start at multiples of 8 rows
-  const int lchunk = (lane % kChunks) ^ lrow_xor;
+  // logical chunk this lane fetches for DMA block i of this wave
+  auto dma_chunk = [&](int i) {
+    const int row = (wave * kBlocksPerWave + i) * kBlockRows + lrow;
+    return (lane % kChunks) ^ row_xor(row);
+  };
   const bool k_tail = (d % kSliceK) != 0;
-  const char* hp[kBlocksPerWave];
+  const int64_t row_bytes = d * kEsz;
+  // Per-lane byte offsets (row start + 16-byte chunk) of this wave's DMA
+  // blocks; a call never spans more than 4 GiB of either operand.
+  uint32_t hoff[kBlocksPerWave];
 #pragma unroll
   for (int i = 0; i < kBlocksPerWave; ++i) {
-    int64_t e = rt * kTileN + wave * 64 + i * kBlockRows + lrow;
+    int64_t e = rt * kTileN + wave * (kTileN / kWaves) + i * kBlockRows + lrow;
     e = e < n_s ? e : n_s - 1;
-    hp[i] = hbase + static_cast<int64_t>(p.rows[e]) * d * kEsz;
+    hoff[i] = static_cast<uint32_t>(static_cast<int64_t>(p.rows[e]) * row_bytes + dma_chunk(i) * 16);
   }
-  const char* wp[kBlocksPerWave];
+  uint32_t woff[kBlocksPerWave];
+  uint64_t wtile = 0;   // address of the current V-tile's first row (uniform)
   auto set_w = [&](int64_t vt) {
+    wtile = reinterpret_cast<uint64_t>(wbase) + static_cast<uint64_t>(vt * kTileV * row_bytes);
 #pragma unroll
     for (int i = 0; i < kBlocksPerWave; ++i) {
-      int64_t v = vt * kTileV + wave * 64 + i * kBlockRows + lrow;
+      int64_t v = vt * kTileV + wave * (kTileV / kWaves) + i * kBlockRows + lrow;
       v = v < V ? v : V - 1;
-      wp[i] = wbase + v * d * kEsz;
+      woff[i] = static_cast<uint32_t>((v - vt * kTileV) * row_bytes + dma_chunk(i) * 16);
     }
   };
   const uint32_t lds_base = static_cast<uint32_t>(
@@ -248,22 +281,30 @@ __global__ __launch_bounds__(kThreads, 1) void lmhead_logprob_kernel(LmheadArgs 
   };
   // DMA j (0 .. kDmaPerSlice-1) of K-slice `slice`; j < kBlocksPerWave are W
   // blocks, the rest hidden-state blocks.  prep_issue() must run first.
-  int64_t issue_koff = 0;
+  uint32_t issue_kbytes = 0;
   int issue_stage = 0;
+  bool issue_tail = false;
   auto prep_issue = [&](int slice) {
     issue_stage = slice % kStages;
     const int kt = slice % nk;
     if (kt == 0) set_w(vt0 + slice / nk);
-    int64_t koff = static_cast<int64_t>(kt) * kSliceK + lchunk * M::kElemsPer16B;
-    if (k_tail && koff >= d) koff = 0;   // in-bounds dummy; zeroed after arrival
-    issue_koff = koff * kEsz;
+    issue_kbytes = static_cast<uint32_t>(kt) * kSliceK * kEsz;
+    issue_tail = k_tail && kt == nk - 1;
   };
   auto issue_one = [&](int j) {
-    if (j < kBlocksPerWave)
-      dma16(wp[j] + issue_koff, lds_addr(issue_stage, 0, wave * kBlocksPerWave + j));
-    else
-      dma16(hp[j - kBlocksPerWave] + issue_koff,
-            lds_addr(issue_stage, 1, wave * kBlocksPerWave + j - kBlocksPerWave));
+    const int i = j % kBlocksPerWave;
+    const uint32_t off = j < kBlocksPerWave ? woff[i] : hoff[i];
+    const uint64_t base = j < kBlocksPerWave ? wtile : reinterpret_cast<uint64_t>(hbase);
+    const uint32_t lds = lds_addr(issue_stage, j < kBlocksPerWave ? 0 : 1, wave * kBlocksPerWave + i);
+    if (!issue_tail) {
+      dma16(base + issue_kbytes, off, lds);
+    } else {
+      // chunks past the end of the row fetch the row start instead (an
+      // in-bounds dummy, zeroed after arrival)
+      const uint32_t chunk_bytes = dma_chunk(i) * 16;
+      const bool in = static_cast<int64_t>(issue_kbytes + chunk_bytes) < row_bytes;
+      dma16(base, off - chunk_bytes + (in ? issue_kbytes + chunk_bytes : 0), lds);
+    }
   };
   auto issue = [&](int slice) {
     prep_issue(slice);
@@ -286,12 +327,12 @@ __global__ __launch_bounds__(kThreads, 1) void lmhead_logprob_kernel(LmheadArgs 
       }
     }
   };
-  auto load_frags = [&](int slice, int kk, uint4 (&fa)[4], uint4 (&fb)[4]) {
+  auto load_frags = [&](int slice, int kk, uint4 (&fa)[4], uint4 (&fb)[kNB]) {
     const int stage = slice % kStages;
 #pragma unroll
     for (int bm = 0; bm < 4; ++bm) fa[bm] = lds[stage][0][swz(wm * 128 + bm * 32 + col, kk * 2 + half)];
 #pragma unroll
-    for (int bn = 0; bn < 4; ++bn) fb[bn] = lds[stage][1][swz(wn * 128 + bn * 32 + col, kk * 2 + half)];
+    for (int bn = 0; bn < kNB; ++bn) fb[bn] = lds[stage][1][swz(wn * kWaveN + bn * 32 + col, kk * 2 + half)];
   };
 
   // Online max / sum-of-exp update of one V-tile, then capture of the
@@ -301,7 +342,7 @@ __global__ __launch_bounds__(kThreads, 1) void lmhead_logprob_kernel(LmheadArgs 
     constexpr bool kMasked = decltype(masked_tag)::value;
     const int64_t vbase = vt * kTileV + wm * 128;   // first vocab row of this wave
 #pragma unroll
-    for (int bn = 0; bn < 4; ++bn) {
+    for (int bn = 0; bn < kNB; ++bn) {
       if (kMasked) {
 #pragma unroll
         for (int bm = 0; bm < 4; ++bm)
@@ -347,7 +388,7 @@ __global__ __launch_bounds__(kThreads, 1) void lmhead_logprob_kernel(LmheadArgs 
 #pragma unroll
     for (int bm = 0; bm < 4; ++bm)
 #pragma unroll
-      for (int bn = 0; bn < 4; ++bn)
+      for (int bn = 0; bn < kNB; ++bn)
 #pragma unroll
         for (int q = 0; q < 16; ++q) acc[bm][bn][q] = 0.f;
   };
@@ -359,13 +400,13 @@ __global__ __launch_bounds__(kThreads, 1) void lmhead_logprob_kernel(LmheadArgs 
   raw_barrier();
   if (k_tail && nk == 1) { clear_k_tail(0); raw_barrier(); }
 
-  // 16 MFMAs of one sub-step.
-  auto mfma_step = [&](const uint4 (&a)[4], const uint4 (&b)[4]) {
+  // The 4 x kNB MFMAs of one sub-step.
+  auto mfma_step = [&](const uint4 (&a)[4], const uint4 (&b)[kNB]) {
 #pragma unroll
-    for (int j = 0; j < 16; ++j) M::run(a[j >> 2], b[j & 3], acc[j >> 2][j & 3]);
+    for (int j = 0; j < 4 * kNB; ++j) M::run(a[j / kNB], b[j % kNB], acc[j / kNB][j % kNB]);
   };
 
-  uint4 fa[2][4], fb[2][4];
+  uint4 fa[2][4], fb[2][kNB];
   int it = 0;   // global slice counter
   for (int64_t vt = vt0; vt < vt1; ++vt) {
     load_frags(it, 0, fa[0], fb[0]);
@@ -396,7 +437,7 @@ __global__ __launch_bounds__(kThreads, 1) void lmhead_logprob_kernel(LmheadArgs 
 
   // ---- merge the two lane halves, then the two vocabulary waves -----------
 #pragma unroll
-  for (int bn = 0; bn < 4; ++bn) {
+  for (int bn = 0; bn < kNB; ++bn) {
     const float m2 = __shfl_xor(run_m[bn], 32);
     const float s2 = __shfl_xor(run_s[bn], 32);
     const float z2 = __shfl_xor(run_z[bn], 32);
@@ -407,8 +448,8 @@ __global__ __launch_bounds__(kThreads, 1) void lmhead_logprob_kernel(LmheadArgs 
   float* xz = xs + kTileN;
   if (wm == 1 && half == 0) {
 #pragma unroll
-    for (int bn = 0; bn < 4; ++bn) {
-      const int tcol = wn * 128 + bn * 32 + col;
+    for (int bn = 0; bn < kNB; ++bn) {
+      const int tcol = wn * kWaveN + bn * 32 + col;
       xm[tcol] = run_m[bn];
       xs[tcol] = run_s[bn];
       xz[tcol] = run_z[bn];
@@ -417,8 +458,8 @@ __global__ __launch_bounds__(kThreads, 1) void lmhead_logprob_kernel(LmheadArgs 
   __syncthreads();
   if (wm == 0 && half == 0) {
 #pragma unroll
-    for (int bn = 0; bn < 4; ++bn) {
-      const int tcol = wn * 128 + bn * 32 + col;
+    for (int bn = 0; bn < kNB; ++bn) {
+      const int tcol = wn * kWaveN + bn * 32 + col;
       float m = run_m[bn], s = run_s[bn], z = run_z[bn];
       combine(m, s, z, xm[tcol], xs[tcol], xz[tcol]);
       const int64_t e = rt * kTileN + tcol;
