@@ -291,12 +291,13 @@ __global__ __launch_bounds__(kThreads, 1) void lmhead_logprob_kernel(LmheadArgs 
     issue_kbytes = static_cast<uint32_t>(kt) * kSliceK * kEsz;
     issue_tail = k_tail && kt == nk - 1;
   };
-  auto issue_one = [&](int j) {
+  auto issue_one = [&](int j, auto tail_tag) {
+    constexpr bool kTail = decltype(tail_tag)::value;
     const int i = j % kBlocksPerWave;
     const uint32_t off = j < kBlocksPerWave ? woff[i] : hoff[i];
     const uint64_t base = j < kBlocksPerWave ? wtile : reinterpret_cast<uint64_t>(hbase);
     const uint32_t lds = lds_addr(issue_stage, j < kBlocksPerWave ? 0 : 1, wave * kBlocksPerWave + i);
-    if (!issue_tail) {
+    if (!kTail) {
       dma16(base + issue_kbytes, off, lds);
     } else {
       // chunks past the end of the row fetch the row start instead (an
@@ -308,8 +309,13 @@ __global__ __launch_bounds__(kThreads, 1) void lmhead_logprob_kernel(LmheadArgs 
   };
   auto issue = [&](int slice) {
     prep_issue(slice);
+    if (!issue_tail) {
 #pragma unroll
-    for (int j = 0; j < kDmaPerSlice; ++j) issue_one(j);
+      for (int j = 0; j < kDmaPerSlice; ++j) issue_one(j, std::false_type{});
+    } else {
+#pragma unroll
+      for (int j = 0; j < kDmaPerSlice; ++j) issue_one(j, std::true_type{});
+    }
   };
 
   // On the last K-slice of a row whose length is not a multiple of the
@@ -417,16 +423,22 @@ __global__ __launch_bounds__(kThreads, 1) void lmhead_logprob_kernel(LmheadArgs 
         const int cur = kk & 1;
         if (kk + 1 < kSub) {
           load_frags(it, kk + 1, fa[cur ^ 1], fb[cur ^ 1]);
-        } else if (it + 1 < n_iter) {
+        } else {
           // every read of slice `it` is issued: wait for slice it+1, then
-          // recycle this slice's stage for slice it+kStages
+          // recycle this slice's stage for slice it+kStages.  On the call's
+          // last slice this waits for nothing and the fragment reads below
+          // fetch stale (in-bounds, unused) LDS: keeping this path
+          // unconditional leaves no control-flow join before the MFMAs.
           const int after = n_iter - 2 - it;
           wait_dma(after < kStages - 2 ? after : kStages - 2);
           raw_barrier();
           if (k_tail && ((it + 1) % nk) == nk - 1) { clear_k_tail(it + 1); raw_barrier(); }
           if (it + kStages < n_iter) issue(it + kStages);
-          if (!last_k) load_frags(it + 1, 0, fa[cur ^ 1], fb[cur ^ 1]);
+          load_frags(it + 1, 0, fa[cur ^ 1], fb[cur ^ 1]);
         }
+        // keep the fragment reads for the next sub-step ahead of this
+        // sub-step's MFMAs, so their LDS latency hides under matrix work
+        __builtin_amdgcn_sched_barrier(0);
         mfma_step(fa[cur], fb[cur]);
       }
     }
