@@ -177,7 +177,10 @@ __device__ __forceinline__ void combine(float& m, float& s, float& z, float m2, 
 // row = 8*(i/4) + 4*(l/32) + (i%4), column = l%32.
 __device__ __forceinline__ int acc_row(int i, int half) { return 8 * (i >> 2) + 4 * half + (i & 3); }
 
-template <bool BF16>
+// KTAIL: d is not a multiple of the K-slice, so the last slice of every
+// row needs zero-filling (a separate instantiation keeps that work out of the
+// common case).
+template <bool BF16, bool KTAIL>
 __global__ __launch_bounds__(kThreads, 1) void lmhead_logprob_kernel(LmheadArgs p) {
   using M = Mma<BF16>;
   constexpr int kEsz = BF16 ? 2 : 4;
@@ -251,7 +254,7 @@ __global__ __launch_bounds__(kThreads, 1) void lmhead_logprob_kernel(LmheadArgs 
     const int row = (wave * kBlocksPerWave + i) * kBlockRows + lrow;
     return (lane % kChunks) ^ row_xor(row);
   };
-  const bool k_tail = (d % kSliceK) != 0;
+  constexpr bool k_tail = KTAIL;
   const int64_t row_bytes = d * kEsz;
   // Per-lane byte offsets (row start + 16-byte chunk) of this wave's DMA
   // blocks; a call never spans more than 4 GiB of either operand.
@@ -423,7 +426,11 @@ __global__ __launch_bounds__(kThreads, 1) void lmhead_logprob_kernel(LmheadArgs 
         const int cur = kk & 1;
         if (kk + 1 < kSub) {
           load_frags(it, kk + 1, fa[cur ^ 1], fb[cur ^ 1]);
-        } else {
+          // keep the fragment reads for the next sub-step ahead of this
+          // sub-step's MFMAs, so their LDS latency hides under matrix work
+          __builtin_amdgcn_sched_barrier(0);
+          mfma_step(fa[cur], fb[cur]);
+        } else if (KTAIL) {
           // every read of slice `it` is issued: wait for slice it+1, then
           // recycle this slice's stage for slice it+kStages.  On the call's
           // last slice this waits for nothing and the fragment reads below
@@ -432,19 +439,38 @@ __global__ __launch_bounds__(kThreads, 1) void lmhead_logprob_kernel(LmheadArgs 
           const int after = n_iter - 2 - it;
           wait_dma(after < kStages - 2 ? after : kStages - 2);
           raw_barrier();
-          if (k_tail && ((it + 1) % nk) == nk - 1) { clear_k_tail(it + 1); raw_barrier(); }
+          if (((it + 1) % nk) == nk - 1) { clear_k_tail(it + 1); raw_barrier(); }
           if (it + kStages < n_iter) issue(it + kStages);
           load_frags(it + 1, 0, fa[cur ^ 1], fb[cur ^ 1]);
+          __builtin_amdgcn_sched_barrier(0);
+          mfma_step(fa[cur], fb[cur]);
+        } else {
+          // As above, but the DMAs for slice it+kStages are spread between
+          // this sub-step's MFMAs so their issue overlaps matrix work.  They
+          // are unconditional: past the end of the work item they re-fetch
+          // the last slice into the stage just freed, which nothing reads.
+          wait_dma(kStages - 2);
+          raw_barrier();
+          const int nxt = it + kStages < n_iter ? it + kStages : n_iter - 1;
+          prep_issue(nxt);
+          load_frags(it + 1, 0, fa[cur ^ 1], fb[cur ^ 1]);
+          __builtin_amdgcn_sched_barrier(0);
+          constexpr int kM = 4 * kNB;                          // MFMAs per sub-step
+          constexpr int kEvery = kM / kDmaPerSlice > 0 ? kM / kDmaPerSlice : 1;
+#pragma unroll
+          for (int j = 0; j < kM; ++j) {
+            M::run(fa[cur][j / kNB], fb[cur][j % kNB], acc[j / kNB][j % kNB]);
+            if (j % kEvery == kEvery - 1 && j / kEvery < kDmaPerSlice) issue_one(j / kEvery, std::false_type{});
+          }
+#pragma unroll
+          for (int j = kM / kEvery; j < kDmaPerSlice; ++j) issue_one(j, std::false_type{});
         }
-        // keep the fragment reads for the next sub-step ahead of this
-        // sub-step's MFMAs, so their LDS latency hides under matrix work
-        __builtin_amdgcn_sched_barrier(0);
-        mfma_step(fa[cur], fb[cur]);
       }
     }
     if ((vt + 1) * kTileV <= V) epilogue(vt, std::false_type{});
     else epilogue(vt, std::true_type{});
   }
+  wait_vmcnt<0>();   // (dummy DMAs past the end may still be landing)
   __syncthreads();
 
   // ---- merge the two lane halves, then the two vocabulary waves -----------
@@ -513,12 +539,15 @@ __global__ __launch_bounds__(256) void merge_kernel(LmheadArgs p, float* __restr
 
 hipError_t launch_lmhead(const LmheadArgs& a, int64_t grid, bool bf16, hipStream_t stream) {
   if (grid <= 0) return hipSuccess;
-  if (bf16)
-    hipLaunchKernelGGL(lmhead_logprob_kernel<true>, dim3(static_cast<unsigned>(grid)), dim3(kThreads),
-                       0, stream, a);
-  else
-    hipLaunchKernelGGL(lmhead_logprob_kernel<false>, dim3(static_cast<unsigned>(grid)), dim3(kThreads),
-                       0, stream, a);
+  const dim3 g(static_cast<unsigned>(grid)), b(kThreads);
+  const bool tail = (a.d % (bf16 ? 8 * kChunks : 4 * kChunks)) != 0;
+  if (bf16) {
+    if (tail) hipLaunchKernelGGL((lmhead_logprob_kernel<true, true>), g, b, 0, stream, a);
+    else hipLaunchKernelGGL((lmhead_logprob_kernel<true, false>), g, b, 0, stream, a);
+  } else {
+    if (tail) hipLaunchKernelGGL((lmhead_logprob_kernel<false, true>), g, b, 0, stream, a);
+    else hipLaunchKernelGGL((lmhead_logprob_kernel<false, false>), g, b, 0, stream, a);
+  }
   return hipGetLastError();
 }
 
