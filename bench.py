@@ -57,6 +57,20 @@ def measured_traffic(workload: str):
     return rec.get("hbm_bytes_per_launch")
 
 
+def mfma_ceiling():
+    """Run the built MFMA ceiling microbenchmark (paper_2609_36864_amd/mfma_ceiling)
+    in a child process; returns its JSON record or None if it is not built."""
+    import subprocess
+    exe = os.path.join(ROOT, "paper_2609_36864_amd", "mfma_ceiling")
+    if not os.path.exists(exe):
+        return None
+    r = subprocess.run([exe], capture_output=True, text=True, timeout=120)
+    if r.returncode != 0:
+        log(f"mfma_ceiling failed: {r.stderr.strip()}")
+        return None
+    return json.loads(r.stdout.strip().splitlines()[-1])
+
+
 def cpu_baseline(w, budget_s: float = 15.0, max_rows: int = 4096):
     """Time the float64 oracle on a seeded sample of eligible rows (both
     contexts) on the host cores; return oracle scored tokens/s."""
@@ -102,6 +116,8 @@ def main() -> int:
     ap.add_argument("--workload", default="c2", help="tiny | c2 | c3 | c4 | c5 (default c2)")
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--cpu-budget", type=float, default=15.0)
+    ap.add_argument("--no-mfma-ceiling", action="store_true",
+                    help="skip measuring this GPU's MFMA ceilings (const/random operands)")
     ap.add_argument("--copy-probe-mb", type=int, default=0,
                     help="after timing, copy this many MiB device-to-device once (a known-size "
                          "kernel that calibrates rocprofv3 FETCH_SIZE / WRITE_SIZE)")
@@ -210,6 +226,12 @@ def main() -> int:
         dst.copy_(src)
         torch.cuda.synchronize()
         log(f"copy probe: {args.copy_probe_mb} MiB device-to-device")
+    if c.dtype == "bf16" and not args.no_mfma_ceiling:
+        ceil = mfma_ceiling()
+        if ceil is not None:
+            ceil["frac_of_random_operand_ceiling"] = achieved / ceil["random_operands_tflops"]
+            result["roofline"]["measured_ceiling"] = ceil
+            log(f"MFMA ceilings: {ceil}")
     traffic = measured_traffic(args.workload)
     if traffic is not None:
         result["roofline"]["traffic"] = traffic

@@ -14,6 +14,7 @@ import sys
 PKG_DIR = os.path.dirname(os.path.abspath(__file__))
 ROOT = os.path.dirname(PKG_DIR)
 LIB_PATH = os.path.join(PKG_DIR, "libhdl.so")
+CEILING_PATH = os.path.join(PKG_DIR, "mfma_ceiling")
 ARCH = "gfx950"
 
 HIP_FLAGS = [
@@ -28,10 +29,9 @@ def sources():
     return sorted(glob.glob(os.path.join(PKG_DIR, "csrc", "*.hip")))
 
 
-def build_library(verbose: bool = False) -> str:
+def _hipcc(args, verbose):
     hipcc = shutil.which("hipcc") or "/opt/rocm/bin/hipcc"
-    tmp = LIB_PATH + ".tmp"
-    cmd = [hipcc, *HIP_FLAGS, "-I", os.path.join(ROOT, "include"), *sources(), "-o", tmp]
+    cmd = [hipcc, *args]
     if verbose:
         print(" ".join(cmd), flush=True)
     r = subprocess.run(cmd, capture_output=True, text=True)
@@ -43,9 +43,24 @@ def build_library(verbose: bool = False) -> str:
         raise RuntimeError(f"hipcc failed ({r.returncode}):\n{err}")
     if verbose and err.strip():
         print(err, file=sys.stderr)
+
+
+def build_ceiling_tool(verbose: bool = False) -> str:
+    """The MFMA ceiling microbenchmark used by bench.py --mfma-ceiling."""
+    tmp = CEILING_PATH + ".tmp"
+    flags = [f for f in HIP_FLAGS if f not in ("-fPIC", "-shared")]
+    _hipcc([*flags, os.path.join(PKG_DIR, "csrc", "tools", "mfma_ceiling.hip"), "-o", tmp], verbose)
+    os.replace(tmp, CEILING_PATH)
+    return CEILING_PATH
+
+
+def build_library(verbose: bool = False) -> str:
+    tmp = LIB_PATH + ".tmp"
+    _hipcc([*HIP_FLAGS, "-I", os.path.join(ROOT, "include"), *sources(), "-o", tmp], verbose)
     os.replace(tmp, LIB_PATH)
     return LIB_PATH
 
 
 if __name__ == "__main__":
     print(build_library(verbose=True))
+    print(build_ceiling_tool(verbose=True))
