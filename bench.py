@@ -29,6 +29,8 @@ if ROOT not in sys.path:
 
 PEAK_TFLOPS = {"bf16": 2500.0, "f32": 157.3}   # MI355X dense MFMA (fp32: matrix fp32 peak)
 METRIC = "scored tokens/sec (both contexts) + MFMA util of fused lm-head logprob kernel"
+# The Entropy localization baseline (Sec. 4.1) scores the original context only.
+METRIC_ENTROPY = "scored tokens/sec (original context) of fused lm-head entropy + top-k (Entropy baseline)"
 
 
 def log(msg: str) -> None:
@@ -71,9 +73,10 @@ def mfma_ceiling():
     return json.loads(r.stdout.strip().splitlines()[-1])
 
 
-def cpu_baseline(w, budget_s: float = 15.0, max_rows: int = 4096):
+def cpu_baseline(w, budget_s: float = 15.0, max_rows: int = 4096, entropy: bool = False):
     """Time the float64 oracle on a seeded sample of eligible rows (both
-    contexts) on the host cores; return oracle scored tokens/s."""
+    contexts; the original context only for the entropy selector) on the host
+    cores; return oracle scored tokens/s."""
     import numpy as np
     import torch
     from oracle import hdl_oracle as O
@@ -90,6 +93,8 @@ def cpu_baseline(w, budget_s: float = 15.0, max_rows: int = 4096):
     hidden = w.rows_hidden()
     tokens = w.rows_tokens().numpy()
     elig = np.nonzero(w.rows_mask().numpy())[0]
+    if entropy:
+        elig = elig[elig < c.R * c.T]
     rng = np.random.default_rng(12345)
     sample = rng.permutation(elig)[:max_rows]
     done, t_total, blk = 0, 0.0, 64
@@ -100,12 +105,16 @@ def cpu_baseline(w, budget_s: float = 15.0, max_rows: int = 4096):
         else:
             H = hidden[torch.as_tensor(rows)].double().numpy()
         t0 = time.perf_counter()
-        O.token_logprobs(H, Wd, tokens[rows])
+        if entropy:
+            O.token_entropy(H, Wd)
+        else:
+            O.token_logprobs(H, Wd, tokens[rows])
         t_total += time.perf_counter() - t0
         done += len(rows)
     return {"value": done / t_total, "unit": "scored tokens/s", "cores": cores, "kind": "oracle",
-            "sample": f"{done} eligible rows drawn from both contexts of this workload "
-                      f"(float64 lm-head log-softmax, {t_total:.1f} s)"}
+            "sample": f"{done} eligible rows drawn from "
+                      f"{'the original context' if entropy else 'both contexts'} of this workload "
+                      f"(float64 lm-head {'entropy' if entropy else 'log-softmax'}, {t_total:.1f} s)"}
 
 
 def main() -> int:
@@ -114,6 +123,9 @@ def main() -> int:
     ap.add_argument("--steps", type=int, default=20)
     ap.add_argument("--warmup", type=int, default=3)
     ap.add_argument("--workload", default="c2", help="tiny | c2 | c3 | c4 | c5 (default c2)")
+    ap.add_argument("--selector", default="hdl", choices=["hdl", "entropy"],
+                    help="hdl: both contexts, |delta log p| top-k (default); entropy: the Entropy "
+                         "baseline, next-token entropy of the original context and its top-k")
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--cpu-budget", type=float, default=15.0)
     ap.add_argument("--no-mfma-ceiling", action="store_true",
@@ -145,20 +157,27 @@ def main() -> int:
     c = w.cfg
     log(f"generated workload {args.workload} in {time.time() - t0:.1f} s")
 
-    hidden = w.rows_hidden().to(dev)
+    ent_sel = args.selector == "entropy"
+    n_keep = c.R * c.T if ent_sel else 2 * c.R * c.T   # rows are [context][root][t]
+    hidden = w.rows_hidden()[:n_keep].to(dev)
     W = w.W.to(dev)
-    tokens = w.rows_tokens().to(dev)
-    mask = w.rows_mask().to(dev)
+    tokens = w.rows_tokens()[:n_keep].to(dev)
+    mask = w.rows_mask()[:n_keep].to(dev)
     mask_rt = w.mask.to(dev)
     n_rows = hidden.shape[0]
     n_scored = int(mask.sum().item())
     dt = hdl.HDL_BF16 if c.dtype == "bf16" else hdl.HDL_F32
     ws = torch.empty(hdl.workspace_size(n_rows, c.d, c.V, dt), dtype=torch.uint8, device=dev)
     logp = torch.empty(n_rows, dtype=torch.float32, device=dev)
+    ent = torch.empty(n_rows, dtype=torch.float32, device=dev)
     torch.cuda.synchronize()
     log(f"inputs resident on {torch.cuda.get_device_name(0)}: {n_rows} rows, {n_scored} scored")
 
     def step():
+        if ent_sel:
+            hdl.token_logprobs(hidden, W, tokens, mask, logp=logp, want_lse=False,
+                               want_entropy=True, entropy=ent, workspace=ws)
+            return hdl.select_top_k(ent.view(c.R, c.T), mask_rt, c.k) + (None,)
         hdl.token_logprobs(hidden, W, tokens, mask, logp=logp, want_lse=False, workspace=ws)
         lp = logp.view(2, c.R, c.T)
         return hdl.select_branch_points(lp[0], lp[1], mask_rt, c.k)
@@ -192,6 +211,8 @@ def main() -> int:
         raise RuntimeError("selection produced an invalid count")
     if not torch.isfinite(logp[mask.bool()]).all():
         raise RuntimeError("non-finite log-probabilities")
+    if ent_sel and not torch.isfinite(ent[mask.bool()]).all():
+        raise RuntimeError("non-finite entropies")
 
     value = n_scored / (step_ms / 1e3)
     flops = 2.0 * c.d * c.V * n_scored
@@ -199,7 +220,7 @@ def main() -> int:
     achieved = flops / (kern_avg_ms / 1e3) / 1e12
     peak = PEAK_TFLOPS[c.dtype]
     result = {
-        "metric": METRIC,
+        "metric": METRIC_ENTROPY if ent_sel else METRIC,
         "value": value,
         "unit": "scored tokens/s",
         "n_gpus": 1,
@@ -212,7 +233,7 @@ def main() -> int:
         "dtype": c.dtype,
         "data": "synthetic (seeded generator; random lm-head weights and hidden states)",
         "config": {"workload": f"{args.workload}: {workloads.DESCRIPTIONS[args.workload]}",
-                   "roots": c.R, "T": c.T, "d": c.d, "V": c.V, "k": c.k,
+                   "selector": args.selector, "roots": c.R, "T": c.T, "d": c.d, "V": c.V, "k": c.k,
                    "scored_tokens_per_step": n_scored},
         "roofline": {"bound": "mfma", "achieved": achieved, "peak": peak, "unit": "TFLOP/s",
                      "frac": achieved / peak, "traffic": None,
@@ -232,12 +253,12 @@ def main() -> int:
             ceil["frac_of_random_operand_ceiling"] = achieved / ceil["random_operands_tflops"]
             result["roofline"]["measured_ceiling"] = ceil
             log(f"MFMA ceilings: {ceil}")
-    traffic = measured_traffic(args.workload)
+    traffic = None if ent_sel else measured_traffic(args.workload)
     if traffic is not None:
         result["roofline"]["traffic"] = traffic
     if not args.no_cpu_baseline:
         log("timing the float64 oracle on a bounded sample")
-        result["cpu_baseline"] = cpu_baseline(w, budget_s=args.cpu_budget)
+        result["cpu_baseline"] = cpu_baseline(w, budget_s=args.cpu_budget, entropy=ent_sel)
     print(json.dumps(result), flush=True)
     return 0
 

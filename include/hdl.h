@@ -88,12 +88,34 @@ size_t hdl_token_logprobs_workspace_size(int64_t n_rows, int64_t d, int64_t voca
  *                        256-byte aligned; contents on entry are ignored.
  *
  * Deterministic: the same inputs give bitwise-identical outputs, and a row's
- * result does not depend on the other rows of the call.
+ * result does not depend on the other rows of the call.  Calls whose hidden
+ * states span more than 4 GiB are processed in several launches internally.
  */
 int hdl_token_logprobs(const void* hidden, const void* w_vocab, const int32_t* tokens,
                        const uint8_t* mask, int64_t n_rows, int64_t d, int64_t vocab,
                        int dtype, float* logp, float* lse_out, void* workspace,
                        size_t workspace_bytes, void* stream);
+
+/*
+ * hdl_token_logprobs plus the next-token entropy of every scored row,
+ *
+ *     entropy[n] = - sum_v p_n(v) log p_n(v) = ln S_n - E_{p_n}[z - m_n],
+ *     S_n = sum_v exp(z_v - m_n),  m_n = max_v z_v,
+ *
+ * accumulated in the same pass over W (one more online accumulator,
+ * sum_v exp(z_v - m) (z_v - m), carried relative to the running max so that
+ * both terms are non-negative and nothing cancels for large logits).  The Entropy localization baseline the paper
+ * compares against ranks positions by this quantity under the original
+ * context (Sec. 4.1, "Rollout protocols"; Table 4).
+ *
+ *  entropy  [n_rows] fp32 out (required; 0 for masked rows).  All other
+ *           arguments, the workspace size and the error behaviour are those
+ *           of hdl_token_logprobs.
+ */
+int hdl_token_logprobs_entropy(const void* hidden, const void* w_vocab, const int32_t* tokens,
+                               const uint8_t* mask, int64_t n_rows, int64_t d, int64_t vocab,
+                               int dtype, float* logp, float* lse_out, float* entropy,
+                               void* workspace, size_t workspace_bytes, void* stream);
 
 /*
  * Hindsight-divergence score and per-root branch-point selection (Eq. 2 and
@@ -119,6 +141,19 @@ int hdl_select_branch_points(const float* logp_orig, const float* logp_hind,
                              const uint8_t* mask, int64_t n_roots, int64_t T, int32_t k,
                              int32_t* idx, float* score, int32_t* count,
                              float* delta_signed, void* stream);
+
+/*
+ * Per-root top-k of an arbitrary per-position value (for example the
+ * next-token entropy of the Entropy baseline, Sec. 4.1): for each root, the
+ * k positions with mask != 0 and a finite value that have the largest value,
+ * ordered (value descending, t ascending); -0 ranks as +0.
+ *
+ *  values [n_roots, T] fp32; mask [n_roots, T] uint8 or NULL; k 1 .. HDL_MAX_K.
+ *  idx [n_roots, k] int32 out (-1 padding), score [n_roots, k] fp32 out
+ *  (0 padding), count [n_roots] int32 out.
+ */
+int hdl_select_top_k(const float* values, const uint8_t* mask, int64_t n_roots, int64_t T,
+                     int32_t k, int32_t* idx, float* score, int32_t* count, void* stream);
 
 /* Static description of a status code. */
 const char* hdl_status_string(int status);

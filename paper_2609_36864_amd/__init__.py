@@ -18,7 +18,7 @@ from typing import Optional, Tuple
 import torch
 
 __all__ = ["HdlError", "HDL_F32", "HDL_BF16", "HDL_MAX_K", "library_path", "load_library",
-           "workspace_size", "token_logprobs", "select_branch_points", "rescore",
+           "workspace_size", "token_logprobs", "select_branch_points", "select_top_k", "rescore",
            "profile_enable", "profile_read", "abi_version"]
 
 HDL_F32 = 0
@@ -54,6 +54,11 @@ def load_library() -> ctypes.CDLL:
     L.hdl_token_logprobs.argtypes = [c_vp, c_vp, c_vp, c_vp, c_i64, c_i64, c_i64, ctypes.c_int,
                                      c_vp, c_vp, c_vp, c_sz, c_vp]
     L.hdl_token_logprobs.restype = ctypes.c_int
+    L.hdl_token_logprobs_entropy.argtypes = [c_vp, c_vp, c_vp, c_vp, c_i64, c_i64, c_i64, ctypes.c_int,
+                                             c_vp, c_vp, c_vp, c_vp, c_sz, c_vp]
+    L.hdl_token_logprobs_entropy.restype = ctypes.c_int
+    L.hdl_select_top_k.argtypes = [c_vp, c_vp, c_i64, c_i64, ctypes.c_int32, c_vp, c_vp, c_vp, c_vp]
+    L.hdl_select_top_k.restype = ctypes.c_int
     L.hdl_select_branch_points.argtypes = [c_vp, c_vp, c_vp, c_i64, c_i64, ctypes.c_int32,
                                            c_vp, c_vp, c_vp, c_vp, c_vp]
     L.hdl_select_branch_points.restype = ctypes.c_int
@@ -116,12 +121,15 @@ def _workspace(device: torch.device, nbytes: int) -> torch.Tensor:
 def token_logprobs(hidden: torch.Tensor, w_vocab: torch.Tensor, tokens: torch.Tensor,
                    mask: Optional[torch.Tensor] = None, *, logp: Optional[torch.Tensor] = None,
                    lse: Optional[torch.Tensor] = None, want_lse: bool = True,
-                   workspace: Optional[torch.Tensor] = None) -> Tuple[torch.Tensor, Optional[torch.Tensor]]:
+                   want_entropy: bool = False, entropy: Optional[torch.Tensor] = None,
+                   workspace: Optional[torch.Tensor] = None):
     """Teacher-forced log p of each row's sampled token (Eq. 1), fused lm-head.
 
     hidden [n_rows, d] and w_vocab [vocab, d], both bf16 or both fp32;
     tokens [n_rows] int32; mask [n_rows] uint8/bool or None.
-    Returns (logp [n_rows] fp32, lse [n_rows] fp32 or None).
+    Returns (logp [n_rows] fp32, lse [n_rows] fp32 or None), or, with
+    want_entropy, (logp, lse, entropy [n_rows] fp32) where entropy is the
+    next-token entropy computed in the same pass.
     """
     L = load_library()
     for name, t in (("hidden", hidden), ("w_vocab", w_vocab), ("tokens", tokens)):
@@ -146,10 +154,18 @@ def token_logprobs(hidden: torch.Tensor, w_vocab: torch.Tensor, tokens: torch.Te
         logp = torch.empty(n_rows, dtype=torch.float32, device=dev)
     if want_lse and lse is None:
         lse = torch.empty(n_rows, dtype=torch.float32, device=dev)
+    if want_entropy and entropy is None:
+        entropy = torch.empty(n_rows, dtype=torch.float32, device=dev)
     nbytes = workspace_size(n_rows, d, vocab, dt)
     if nbytes == 0:
         raise ValueError(f"invalid sizes n_rows={n_rows} d={d} vocab={vocab}")
     ws = workspace if workspace is not None else _workspace(dev, nbytes)
+    if want_entropy:
+        _check(L.hdl_token_logprobs_entropy(hidden.data_ptr(), w_vocab.data_ptr(), tokens.data_ptr(),
+                                            _ptr(mask), n_rows, d, vocab, dt, logp.data_ptr(), _ptr(lse),
+                                            entropy.data_ptr(), ws.data_ptr(),
+                                            ws.numel() * ws.element_size(), _stream_handle(dev)))
+        return logp, lse, entropy
     _check(L.hdl_token_logprobs(hidden.data_ptr(), w_vocab.data_ptr(), tokens.data_ptr(), _ptr(mask),
                                 n_rows, d, vocab, dt, logp.data_ptr(), _ptr(lse), ws.data_ptr(),
                                 ws.numel() * ws.element_size(), _stream_handle(dev)))
@@ -187,6 +203,31 @@ def select_branch_points(logp_orig: torch.Tensor, logp_hind: torch.Tensor,
                                       int(k), idx.data_ptr(), score.data_ptr(), count.data_ptr(),
                                       _ptr(delta), _stream_handle(dev)))
     return idx, score, count, delta
+
+
+def select_top_k(values: torch.Tensor, mask: Optional[torch.Tensor], k: int):
+    """Per-root top-k of a per-position value, e.g. next-token entropy for the
+    Entropy localization baseline (Sec. 4.1).  values [R, T] fp32, mask
+    [R, T] uint8 or None.  Returns (idx [R,k] int32, score [R,k] fp32, count [R] int32)."""
+    L = load_library()
+    _require_cuda("values", values)
+    if values.dtype != torch.float32 or values.dim() != 2:
+        raise ValueError("values must be float32 [R, T]")
+    R, T = values.shape
+    dev = values.device
+    if mask is not None:
+        _require_cuda("mask", mask)
+        if mask.dtype == torch.bool:
+            mask = mask.view(torch.uint8)
+        if mask.dtype != torch.uint8 or tuple(mask.shape) != (R, T):
+            raise ValueError("mask must be uint8 [R, T]")
+    kk = max(int(k), 1)
+    idx = torch.empty(R, kk, dtype=torch.int32, device=dev)
+    score = torch.empty(R, kk, dtype=torch.float32, device=dev)
+    count = torch.empty(R, dtype=torch.int32, device=dev)
+    _check(L.hdl_select_top_k(values.data_ptr(), _ptr(mask), R, T, int(k), idx.data_ptr(),
+                              score.data_ptr(), count.data_ptr(), _stream_handle(dev)))
+    return idx, score, count
 
 
 def rescore(hidden_both: torch.Tensor, w_vocab: torch.Tensor, tokens: torch.Tensor,

@@ -4,7 +4,8 @@
 // each policy-generated token; agent trajectories also contain environment
 // observations, Sec. 4.1).  Compacting the mask first means masked rows cost
 // no matrix work in the fused lm-head kernel.  Masked rows get log p = 0 and
-// lse = 0 here, so every output element is written by exactly one kernel.
+// lse = 0 (and entropy = 0) here, so every output element is written by
+// exactly one kernel.
 //
 // Two launches, both deterministic: per-block counts, then a scan + scatter
 // in which every block sums the counts of the blocks before it.
@@ -69,7 +70,8 @@ __global__ __launch_bounds__(kThreads) void scatter_kernel(const uint8_t* __rest
                                                            int32_t* __restrict__ rows,
                                                            int32_t* __restrict__ n_scored,
                                                            float* __restrict__ logp,
-                                                           float* __restrict__ lse) {
+                                                           float* __restrict__ lse,
+                                                           float* __restrict__ entropy) {
   // rows scored by the blocks before this one
   int part = 0;
   for (int b = threadIdx.x; b < static_cast<int>(blockIdx.x); b += kThreads) part += block_counts[b];
@@ -96,6 +98,7 @@ __global__ __launch_bounds__(kThreads) void scatter_kernel(const uint8_t* __rest
     } else {
       logp[n] = 0.f;
       if (lse) lse[n] = 0.f;
+      if (entropy) entropy[n] = 0.f;
     }
   }
   if (blockIdx.x == gridDim.x - 1 && threadIdx.x == 0) *n_scored = prefix + block_total;
@@ -106,7 +109,7 @@ __global__ __launch_bounds__(kThreads) void scatter_kernel(const uint8_t* __rest
 // Scratch for the per-block counts lives right after n_scored in the
 // workspace (see make_plan in hdl_api.hip).
 hipError_t launch_compact(const uint8_t* mask, int64_t n_rows, int32_t* rows, int32_t* n_scored,
-                          float* logp, float* lse, hipStream_t stream) {
+                          float* logp, float* lse, float* entropy, hipStream_t stream) {
   const int64_t blocks = (n_rows + kPerBlock - 1) / kPerBlock;
   int32_t* block_counts = n_scored + 64;
   hipLaunchKernelGGL(count_kernel, dim3(static_cast<unsigned>(blocks)), dim3(kThreads), 0, stream, mask,
@@ -114,7 +117,7 @@ hipError_t launch_compact(const uint8_t* mask, int64_t n_rows, int32_t* rows, in
   hipError_t e = hipGetLastError();
   if (e != hipSuccess) return e;
   hipLaunchKernelGGL(scatter_kernel, dim3(static_cast<unsigned>(blocks)), dim3(kThreads), 0, stream, mask,
-                     n_rows, block_counts, rows, n_scored, logp, lse);
+                     n_rows, block_counts, rows, n_scored, logp, lse, entropy);
   return hipGetLastError();
 }
 

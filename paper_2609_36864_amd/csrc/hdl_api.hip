@@ -70,7 +70,8 @@ LmheadPlan make_plan(int64_t n_rows_total, int64_t vocab, int64_t d, int esz) {
   p.n_gch = (p.n_ch + kGroupCH - 1) / kGroupCH;
   const int64_t groups = p.n_grt * p.n_gch;
   p.grid = (groups + kNumXcd - 1) / kNumXcd * kNumXcd * (kGroupRT * kGroupCH);
-  // workspace: rows [n_rows] | n_scored + block counts | partials [3][n_ch][n_rows]
+  // workspace: rows [n_rows] | n_scored + block counts | partials [4][n_ch][n_rows]
+  // (max, sum of exp, sampled-token logit, and the entropy accumulator)
   size_t off = 0;
   p.off_rows = off;
   off = round_up(off + sizeof(int32_t) * static_cast<size_t>(n_rows), 256);
@@ -78,7 +79,7 @@ LmheadPlan make_plan(int64_t n_rows_total, int64_t vocab, int64_t d, int esz) {
   const size_t n_blocks = static_cast<size_t>((n_rows + 4095) / 4096);
   off = round_up(off + sizeof(int32_t) * (64 + n_blocks), 256);
   p.off_part = off;
-  off = round_up(off + 3 * sizeof(float) * static_cast<size_t>(p.n_ch) * static_cast<size_t>(n_rows), 256);
+  off = round_up(off + 4 * sizeof(float) * static_cast<size_t>(p.n_ch) * static_cast<size_t>(n_rows), 256);
   p.bytes = off;
   return p;
 }
@@ -95,35 +96,40 @@ size_t hdl_token_logprobs_workspace_size(int64_t n_rows, int64_t d, int64_t voca
   return hdl::make_plan(n_rows, vocab, d, esz).bytes;
 }
 
-int hdl_token_logprobs(const void* hidden, const void* w_vocab, const int32_t* tokens,
-                       const uint8_t* mask, int64_t n_rows, int64_t d, int64_t vocab, int dtype,
-                       float* logp, float* lse_out, void* workspace, size_t workspace_bytes,
-                       void* stream) {
+}  // extern "C"
+
+namespace {
+
+// Shared implementation of hdl_token_logprobs / hdl_token_logprobs_entropy.
+int token_stats(const char* fn, const void* hidden, const void* w_vocab, const int32_t* tokens,
+                const uint8_t* mask, int64_t n_rows, int64_t d, int64_t vocab, int dtype, float* logp,
+                float* lse_out, float* entropy, void* workspace, size_t workspace_bytes,
+                void* stream) {
   g_last_error[0] = '\0';
   if (!hidden || !w_vocab || !tokens || !logp)
-    return fail(HDL_ERR_INVALID_ARG, "hdl_token_logprobs: null hidden, w_vocab, tokens or logp");
+    return fail(HDL_ERR_INVALID_ARG, "%s: null hidden, w_vocab, tokens or logp", fn);
   if (n_rows <= 0 || d <= 0 || vocab <= 0)
-    return fail(HDL_ERR_INVALID_ARG, "hdl_token_logprobs: sizes must be positive (n_rows=%lld d=%lld vocab=%lld)",
-                static_cast<long long>(n_rows), static_cast<long long>(d), static_cast<long long>(vocab));
+    return fail(HDL_ERR_INVALID_ARG, "%s: sizes must be positive (n_rows=%lld d=%lld vocab=%lld)",
+                fn, static_cast<long long>(n_rows), static_cast<long long>(d), static_cast<long long>(vocab));
   if (n_rows > INT32_MAX || vocab > INT32_MAX)
-    return fail(HDL_ERR_UNSUPPORTED, "hdl_token_logprobs: n_rows and vocab must fit in int32");
+    return fail(HDL_ERR_UNSUPPORTED, "%s: n_rows and vocab must fit in int32", fn);
   if (dtype != HDL_F32 && dtype != HDL_BF16)
-    return fail(HDL_ERR_UNSUPPORTED, "hdl_token_logprobs: unknown dtype %d", dtype);
+    return fail(HDL_ERR_UNSUPPORTED, "%s: unknown dtype %d", fn, dtype);
   if (d % 8 != 0)
-    return fail(HDL_ERR_UNSUPPORTED, "hdl_token_logprobs: d=%lld is not a multiple of 8", static_cast<long long>(d));
+    return fail(HDL_ERR_UNSUPPORTED, "%s: d=%lld is not a multiple of 8", fn, static_cast<long long>(d));
   if (!aligned(hidden, 16) || !aligned(w_vocab, 16))
-    return fail(HDL_ERR_INVALID_ARG, "hdl_token_logprobs: hidden and w_vocab must be 16-byte aligned");
+    return fail(HDL_ERR_INVALID_ARG, "%s: hidden and w_vocab must be 16-byte aligned", fn);
   const int esz = dtype == HDL_BF16 ? 2 : 4;
   if (hdl::rows_per_launch(d, esz) < hdl::kTileN)
-    return fail(HDL_ERR_UNSUPPORTED, "hdl_token_logprobs: hidden rows larger than 16 MiB");
+    return fail(HDL_ERR_UNSUPPORTED, "%s: hidden rows larger than 16 MiB", fn);
   const hdl::LmheadPlan plan = hdl::make_plan(n_rows, vocab, d, esz);
   if (!workspace || workspace_bytes < plan.bytes)
-    return fail(HDL_ERR_WORKSPACE, "hdl_token_logprobs: workspace of %zu bytes needed, %zu given",
-                plan.bytes, workspace ? workspace_bytes : static_cast<size_t>(0));
+    return fail(HDL_ERR_WORKSPACE, "%s: workspace of %zu bytes needed, %zu given",
+                fn, plan.bytes, workspace ? workspace_bytes : static_cast<size_t>(0));
   if (!aligned(workspace, 256))
-    return fail(HDL_ERR_INVALID_ARG, "hdl_token_logprobs: workspace must be 256-byte aligned");
+    return fail(HDL_ERR_INVALID_ARG, "%s: workspace must be 256-byte aligned", fn);
   if (plan.grid > INT32_MAX)
-    return fail(HDL_ERR_UNSUPPORTED, "hdl_token_logprobs: problem too large for one launch");
+    return fail(HDL_ERR_UNSUPPORTED, "%s: problem too large for one launch", fn);
 
   hipStream_t s = static_cast<hipStream_t>(stream);
   char* ws = static_cast<char*>(workspace);
@@ -140,7 +146,8 @@ int hdl_token_logprobs(const void* hidden, const void* w_vocab, const int32_t* t
     const hdl::LmheadPlan lp = hdl::make_plan(n, vocab, d, esz);
     float* logp_c = logp + r0;
     float* lse_c = lse_out ? lse_out + r0 : nullptr;
-    hipError_t e = hdl::launch_compact(mask ? mask + r0 : nullptr, n, rows, n_scored, logp_c, lse_c, s);
+    float* ent_c = entropy ? entropy + r0 : nullptr;
+    hipError_t e = hdl::launch_compact(mask ? mask + r0 : nullptr, n, rows, n_scored, logp_c, lse_c, ent_c, s);
     if (e != hipSuccess) return hip_fail(e, "compaction launch");
 
     hdl::LmheadArgs a{};
@@ -159,6 +166,7 @@ int hdl_token_logprobs(const void* hidden, const void* w_vocab, const int32_t* t
     a.part_m = part;
     a.part_s = part + plane;
     a.part_z = part + 2 * plane;
+    a.part_t = entropy ? part + 3 * plane : nullptr;
 
     std::pair<hipEvent_t, hipEvent_t> ev{nullptr, nullptr};
     bool timed = false;
@@ -169,7 +177,7 @@ int hdl_token_logprobs(const void* hidden, const void* w_vocab, const int32_t* t
           ev = g_prof.spare.back();
           g_prof.spare.pop_back();
         } else if (hipEventCreate(&ev.first) != hipSuccess || hipEventCreate(&ev.second) != hipSuccess) {
-          return fail(HDL_ERR_HIP, "hdl_token_logprobs: hipEventCreate failed");
+          return fail(HDL_ERR_HIP, "%s: hipEventCreate failed", fn);
         }
         timed = true;
       }
@@ -182,10 +190,34 @@ int hdl_token_logprobs(const void* hidden, const void* w_vocab, const int32_t* t
       std::lock_guard<std::mutex> lk(g_prof.mu);
       g_prof.pending.push_back(ev);
     }
-    e = hdl::launch_merge(a, n, logp_c, lse_c, s);
+    e = hdl::launch_merge(a, n, logp_c, lse_c, ent_c, s);
     if (e != hipSuccess) return hip_fail(e, "merge kernel launch");
   }
   return HDL_OK;
+}
+
+}  // namespace
+
+extern "C" {
+
+int hdl_token_logprobs(const void* hidden, const void* w_vocab, const int32_t* tokens,
+                       const uint8_t* mask, int64_t n_rows, int64_t d, int64_t vocab, int dtype,
+                       float* logp, float* lse_out, void* workspace, size_t workspace_bytes,
+                       void* stream) {
+  return token_stats("hdl_token_logprobs", hidden, w_vocab, tokens, mask, n_rows, d, vocab, dtype,
+                     logp, lse_out, nullptr, workspace, workspace_bytes, stream);
+}
+
+int hdl_token_logprobs_entropy(const void* hidden, const void* w_vocab, const int32_t* tokens,
+                               const uint8_t* mask, int64_t n_rows, int64_t d, int64_t vocab,
+                               int dtype, float* logp, float* lse_out, float* entropy,
+                               void* workspace, size_t workspace_bytes, void* stream) {
+  if (!entropy) {
+    g_last_error[0] = '\0';
+    return fail(HDL_ERR_INVALID_ARG, "hdl_token_logprobs_entropy: null entropy");
+  }
+  return token_stats("hdl_token_logprobs_entropy", hidden, w_vocab, tokens, mask, n_rows, d, vocab,
+                     dtype, logp, lse_out, entropy, workspace, workspace_bytes, stream);
 }
 
 int hdl_select_branch_points(const float* logp_orig, const float* logp_hind, const uint8_t* mask,
@@ -203,7 +235,24 @@ int hdl_select_branch_points(const float* logp_orig, const float* logp_hind, con
   if (n_roots > INT32_MAX || T > INT32_MAX)
     return fail(HDL_ERR_UNSUPPORTED, "hdl_select_branch_points: n_roots and T must fit in int32");
   hipError_t e = hdl::launch_select(logp_orig, logp_hind, mask, n_roots, T, k, idx, score, count,
-                                    delta_signed, static_cast<hipStream_t>(stream));
+                                    delta_signed, false, static_cast<hipStream_t>(stream));
+  if (e != hipSuccess) return hip_fail(e, "selection kernel launch");
+  return HDL_OK;
+}
+
+int hdl_select_top_k(const float* values, const uint8_t* mask, int64_t n_roots, int64_t T,
+                     int32_t k, int32_t* idx, float* score, int32_t* count, void* stream) {
+  g_last_error[0] = '\0';
+  if (!values || !idx || !score || !count)
+    return fail(HDL_ERR_INVALID_ARG, "hdl_select_top_k: null required pointer");
+  if (n_roots <= 0 || T <= 0)
+    return fail(HDL_ERR_INVALID_ARG, "hdl_select_top_k: n_roots and T must be positive");
+  if (k < 1) return fail(HDL_ERR_INVALID_ARG, "hdl_select_top_k: k=%d must be >= 1", k);
+  if (k > HDL_MAX_K) return fail(HDL_ERR_UNSUPPORTED, "hdl_select_top_k: k=%d exceeds %d", k, HDL_MAX_K);
+  if (n_roots > INT32_MAX || T > INT32_MAX)
+    return fail(HDL_ERR_UNSUPPORTED, "hdl_select_top_k: n_roots and T must fit in int32");
+  hipError_t e = hdl::launch_select(values, nullptr, mask, n_roots, T, k, idx, score, count, nullptr,
+                                    true, static_cast<hipStream_t>(stream));
   if (e != hipSuccess) return hip_fail(e, "selection kernel launch");
   return HDL_OK;
 }
@@ -221,7 +270,7 @@ const char* hdl_status_string(int status) {
 
 const char* hdl_last_error(void) { return g_last_error; }
 
-int hdl_abi_version(void) { return 1; }
+int hdl_abi_version(void) { return 2; }
 
 int hdl_profile_enable(int on) {
   std::lock_guard<std::mutex> lk(g_prof.mu);

@@ -52,16 +52,18 @@ struct LmheadArgs {
   float* part_m;            // running max (natural-log units)
   float* part_s;            // sum of exp(z - m)
   float* part_z;            // sampled-token logit, -inf where not captured
+  float* part_t;            // sum of exp(z - m) * z, or nullptr (no entropy)
 };
 
 hipError_t launch_compact(const uint8_t* mask, int64_t n_rows, int32_t* rows,
-                          int32_t* n_scored, float* logp, float* lse,
+                          int32_t* n_scored, float* logp, float* lse, float* entropy,
                           hipStream_t stream);
 hipError_t launch_lmhead(const LmheadArgs& a, int64_t grid, bool bf16, hipStream_t stream);
 hipError_t launch_merge(const LmheadArgs& a, int64_t n_rows, float* logp, float* lse,
-                        hipStream_t stream);
+                        float* entropy, hipStream_t stream);
+// values == true: rank `lo` itself (lh unused); otherwise rank |lh - lo|.
 hipError_t launch_select(const float* lo, const float* lh, const uint8_t* mask,
                          int64_t n_roots, int64_t T, int k, int32_t* idx, float* score,
-                         int32_t* count, float* delta, hipStream_t stream);
+                         int32_t* count, float* delta, bool values, hipStream_t stream);
 
 }  // namespace hdl

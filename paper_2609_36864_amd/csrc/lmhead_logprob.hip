@@ -162,13 +162,29 @@ template <> struct Mma<false> {
   }
 };
 
-// Combine two (max, sum-of-exp, captured logit) states.  Symmetric in its
-// arguments, so partner lanes obtain bitwise-identical results.
-__device__ __forceinline__ void combine(float& m, float& s, float& z, float m2, float s2, float z2) {
+// t of a state, moved from its own max m to a larger max mn:
+//   sum exp(z - mn) * (z - mn) log2(e) = f * (t + (m - mn) log2(e) * s),  f = exp(m - mn).
+// An empty state (m = -inf, s = t = 0) stays 0.
+__device__ __forceinline__ float shift_t(float t, float s, float m, float mn, float f) {
+  return (m == mn) ? t : (m == kNegInf ? 0.f : f * __builtin_fmaf((m - mn) * kLog2e, s, t));
+}
+
+// Combine two (max m, sum of exp(z - m) s, captured logit z, and for the
+// entropy t = sum exp(z - m) * (z - m) log2(e)) states.  t is only
+// meaningful when entropy is requested; otherwise it stays 0 and the
+// compiler drops it.  t is kept relative to m so that the entropy
+// ln s - ln(2) t / s is a sum of two non-negative terms: no cancellation
+// against the size of the logits.
+__device__ __forceinline__ void combine(float& m, float& s, float& z, float& t, float m2, float s2,
+                                        float z2, float t2) {
   const float mn = fmaxf(m, m2);
-  const float a = (m == mn) ? s : s * fast_exp2((m - mn) * kLog2e);
-  const float b = (m2 == mn) ? s2 : s2 * fast_exp2((m2 - mn) * kLog2e);
-  s = a + b;
+  const float fa = (m == mn) ? 1.f : fast_exp2((m - mn) * kLog2e);
+  const float fb = (m2 == mn) ? 1.f : fast_exp2((m2 - mn) * kLog2e);
+  t = shift_t(t, s, m, mn, fa) + shift_t(t2, s2, m2, mn, fb);
+  // (an explicit fma: a contractible s * fa + s2 * fb could be fused
+  // differently in different instantiations, and log p must not depend on
+  // whether the entropy is requested)
+  s = __builtin_fmaf(s, fa, s2 * fb);
   m = mn;
   z = fmaxf(z, z2);
 }
@@ -179,8 +195,9 @@ __device__ __forceinline__ int acc_row(int i, int half) { return 8 * (i >> 2) + 
 
 // KTAIL: d is not a multiple of the K-slice, so the last slice of every
 // row needs zero-filling (a separate instantiation keeps that work out of the
-// common case).
-template <bool BF16, bool KTAIL>
+// common case).  ENT: also accumulate sum exp(z - m) * (z - m) for the next-token
+// entropy H = ln s - E_p[z - m] (the Entropy localization baseline).
+template <bool BF16, bool KTAIL, bool ENT>
 __global__ __launch_bounds__(kThreads, 1) void lmhead_logprob_kernel(LmheadArgs p) {
   using M = Mma<BF16>;
   constexpr int kEsz = BF16 ? 2 : 4;
@@ -231,9 +248,9 @@ __global__ __launch_bounds__(kThreads, 1) void lmhead_logprob_kernel(LmheadArgs 
     tok[bn] = p.tokens[p.rows[e]];
   }
 
-  float run_m[kNB], run_s[kNB], run_z[kNB];
+  float run_m[kNB], run_s[kNB], run_z[kNB], run_t[kNB];
 #pragma unroll
-  for (int bn = 0; bn < kNB; ++bn) { run_m[bn] = kNegInf; run_s[bn] = 0.f; run_z[bn] = kNegInf; }
+  for (int bn = 0; bn < kNB; ++bn) { run_m[bn] = kNegInf; run_s[bn] = 0.f; run_z[bn] = kNegInf; run_t[bn] = 0.f; }
 
   f32x16_t acc[4][kNB];
 #pragma unroll
@@ -367,16 +384,27 @@ __global__ __launch_bounds__(kThreads, 1) void lmhead_logprob_kernel(LmheadArgs 
       const float mnew = fmaxf(run_m[bn], mx);
       if (!kMasked || mnew != kNegInf) {
         const float mb = mnew * kLog2e;
-        float s4[4];
+        float s4[4], t4[4];
 #pragma unroll
         for (int bm = 0; bm < 4; ++bm) {
-          float sacc = 0.f;
+          float sacc = 0.f, tacc = 0.f;
 #pragma unroll
-          for (int q = 0; q < 16; ++q) sacc += fast_exp2(__builtin_fmaf(acc[bm][bn][q], kLog2e, -mb));
+          for (int q = 0; q < 16; ++q) {
+            const float zq = acc[bm][bn][q];
+            const float zl = __builtin_fmaf(zq, kLog2e, -mb);   // (z - m) log2(e)
+            const float e = fast_exp2(zl);
+            sacc += e;
+            // (masked rows hold -inf and e = 0; their product term is 0)
+            if (ENT) tacc = __builtin_fmaf(e, (kMasked && zq == kNegInf) ? 0.f : zl, tacc);
+          }
           s4[bm] = sacc;
+          t4[bm] = tacc;
         }
         const float tile_sum = (s4[0] + s4[1]) + (s4[2] + s4[3]);
-        run_s[bn] = __builtin_fmaf(run_s[bn], fast_exp2(__builtin_fmaf(run_m[bn], kLog2e, -mb)), tile_sum);
+        const float rescale = fast_exp2(__builtin_fmaf(run_m[bn], kLog2e, -mb));
+        if (ENT)   // (before run_s changes: shift_t wants the old sum)
+          run_t[bn] = shift_t(run_t[bn], run_s[bn], run_m[bn], mnew, rescale) + ((t4[0] + t4[1]) + (t4[2] + t4[3]));
+        run_s[bn] = __builtin_fmaf(run_s[bn], rescale, tile_sum);
         run_m[bn] = mnew;
       }
       const int64_t o = static_cast<int64_t>(tok[bn]) - vbase;
@@ -420,7 +448,6 @@ __global__ __launch_bounds__(kThreads, 1) void lmhead_logprob_kernel(LmheadArgs 
   for (int64_t vt = vt0; vt < vt1; ++vt) {
     load_frags(it, 0, fa[0], fb[0]);
     for (int kt = 0; kt < nk; ++kt, ++it) {
-      const bool last_k = kt == nk - 1;
 #pragma unroll
       for (int kk = 0; kk < kSub; ++kk) {
         const int cur = kk & 1;
@@ -479,11 +506,13 @@ __global__ __launch_bounds__(kThreads, 1) void lmhead_logprob_kernel(LmheadArgs 
     const float m2 = __shfl_xor(run_m[bn], 32);
     const float s2 = __shfl_xor(run_s[bn], 32);
     const float z2 = __shfl_xor(run_z[bn], 32);
-    combine(run_m[bn], run_s[bn], run_z[bn], m2, s2, z2);
+    const float t2 = ENT ? __shfl_xor(run_t[bn], 32) : 0.f;
+    combine(run_m[bn], run_s[bn], run_z[bn], run_t[bn], m2, s2, z2, t2);
   }
   float* xm = reinterpret_cast<float*>(&lds[0][0][0]);
   float* xs = xm + kTileN;
   float* xz = xs + kTileN;
+  float* xt = xz + kTileN;
   if (wm == 1 && half == 0) {
 #pragma unroll
     for (int bn = 0; bn < kNB; ++bn) {
@@ -491,6 +520,7 @@ __global__ __launch_bounds__(kThreads, 1) void lmhead_logprob_kernel(LmheadArgs 
       xm[tcol] = run_m[bn];
       xs[tcol] = run_s[bn];
       xz[tcol] = run_z[bn];
+      if (ENT) xt[tcol] = run_t[bn];
     }
   }
   __syncthreads();
@@ -498,14 +528,15 @@ __global__ __launch_bounds__(kThreads, 1) void lmhead_logprob_kernel(LmheadArgs 
 #pragma unroll
     for (int bn = 0; bn < kNB; ++bn) {
       const int tcol = wn * kWaveN + bn * 32 + col;
-      float m = run_m[bn], s = run_s[bn], z = run_z[bn];
-      combine(m, s, z, xm[tcol], xs[tcol], xz[tcol]);
+      float m = run_m[bn], s = run_s[bn], z = run_z[bn], t = run_t[bn];
+      combine(m, s, z, t, xm[tcol], xs[tcol], xz[tcol], ENT ? xt[tcol] : 0.f);
       const int64_t e = rt * kTileN + tcol;
       if (e < n_s) {
         const int64_t o = ch * p.part_stride + e;
         p.part_m[o] = m;
         p.part_s[o] = s;
         p.part_z[o] = z;
+        if (ENT) p.part_t[o] = t;
       }
     }
   }
@@ -513,15 +544,18 @@ __global__ __launch_bounds__(kThreads, 1) void lmhead_logprob_kernel(LmheadArgs 
 
 // Combine the chunk partials of each scored row in chunk order and write
 // log p = z_y - (m + ln s); non-finite or out-of-range tokens give NaN.
+// With entropy requested, also H = ln s - E_p[z - m] = ln s - ln(2) t / s.
 __global__ __launch_bounds__(256) void merge_kernel(LmheadArgs p, float* __restrict__ logp,
-                                                    float* __restrict__ lse_out) {
+                                                    float* __restrict__ lse_out,
+                                                    float* __restrict__ entropy) {
   const int64_t e = static_cast<int64_t>(blockIdx.x) * blockDim.x + threadIdx.x;
   const int64_t n_s = *p.n_scored;
   if (e >= n_s) return;
-  float m = p.part_m[e], s = p.part_s[e], z = p.part_z[e];
+  const bool ent = p.part_t != nullptr;
+  float m = p.part_m[e], s = p.part_s[e], z = p.part_z[e], t = ent ? p.part_t[e] : 0.f;
   for (int64_t c = 1; c < p.n_ch; ++c) {
     const int64_t o = c * p.part_stride + e;
-    combine(m, s, z, p.part_m[o], p.part_s[o], p.part_z[o]);
+    combine(m, s, z, t, p.part_m[o], p.part_s[o], p.part_z[o], ent ? p.part_t[o] : 0.f);
   }
   const float lse = m + __builtin_amdgcn_logf(s) * 0.6931471805599453f;
   const int row = p.rows[e];
@@ -533,6 +567,12 @@ __global__ __launch_bounds__(256) void merge_kernel(LmheadArgs p, float* __restr
   if (y < 0 || y >= p.vocab) lp = __builtin_nanf("");
   logp[row] = lp;
   if (lse_out) lse_out[row] = lse;
+  if (ent) {
+    // The exact value is >= 0; clamp the rounding residue of a near one-hot
+    // distribution.
+    const float h = __builtin_fmaf(-0.6931471805599453f, t / s, __builtin_amdgcn_logf(s) * 0.6931471805599453f);
+    entropy[row] = h > 0.f ? h : 0.f;
+  }
 }
 
 }  // namespace
@@ -541,21 +581,27 @@ hipError_t launch_lmhead(const LmheadArgs& a, int64_t grid, bool bf16, hipStream
   if (grid <= 0) return hipSuccess;
   const dim3 g(static_cast<unsigned>(grid)), b(kThreads);
   const bool tail = (a.d % (bf16 ? 8 * kChunks : 4 * kChunks)) != 0;
-  if (bf16) {
-    if (tail) hipLaunchKernelGGL((lmhead_logprob_kernel<true, true>), g, b, 0, stream, a);
-    else hipLaunchKernelGGL((lmhead_logprob_kernel<true, false>), g, b, 0, stream, a);
-  } else {
-    if (tail) hipLaunchKernelGGL((lmhead_logprob_kernel<false, true>), g, b, 0, stream, a);
-    else hipLaunchKernelGGL((lmhead_logprob_kernel<false, false>), g, b, 0, stream, a);
+  const bool ent = a.part_t != nullptr;
+  const int which = (bf16 ? 4 : 0) + (tail ? 2 : 0) + (ent ? 1 : 0);
+  switch (which) {
+    case 0: hipLaunchKernelGGL((lmhead_logprob_kernel<false, false, false>), g, b, 0, stream, a); break;
+    case 1: hipLaunchKernelGGL((lmhead_logprob_kernel<false, false, true>), g, b, 0, stream, a); break;
+    case 2: hipLaunchKernelGGL((lmhead_logprob_kernel<false, true, false>), g, b, 0, stream, a); break;
+    case 3: hipLaunchKernelGGL((lmhead_logprob_kernel<false, true, true>), g, b, 0, stream, a); break;
+    case 4: hipLaunchKernelGGL((lmhead_logprob_kernel<true, false, false>), g, b, 0, stream, a); break;
+    case 5: hipLaunchKernelGGL((lmhead_logprob_kernel<true, false, true>), g, b, 0, stream, a); break;
+    case 6: hipLaunchKernelGGL((lmhead_logprob_kernel<true, true, false>), g, b, 0, stream, a); break;
+    default: hipLaunchKernelGGL((lmhead_logprob_kernel<true, true, true>), g, b, 0, stream, a); break;
   }
   return hipGetLastError();
 }
 
 hipError_t launch_merge(const LmheadArgs& a, int64_t n_rows, float* logp, float* lse,
-                        hipStream_t stream) {
+                        float* entropy, hipStream_t stream) {
   const int64_t blocks = (n_rows + 255) / 256;
   if (blocks <= 0) return hipSuccess;
-  hipLaunchKernelGGL(merge_kernel, dim3(static_cast<unsigned>(blocks)), dim3(256), 0, stream, a, logp, lse);
+  hipLaunchKernelGGL(merge_kernel, dim3(static_cast<unsigned>(blocks)), dim3(256), 0, stream, a, logp, lse,
+                     entropy);
   return hipGetLastError();
 }
 

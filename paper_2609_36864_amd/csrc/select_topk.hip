@@ -1,11 +1,15 @@
 // Hindsight-divergence score and per-root branch-point selection (Eq. 2 and
-// the ranking of Sec. 3.2).
+// the ranking of Sec. 3.2), and the same per-root top-k over an arbitrary
+// per-position value (the Entropy localization baseline of Sec. 4.1 ranks
+// positions by next-token entropy).
 //
 // One 1024-thread workgroup per root.  For position t:
 //     delta = logp_hind[t] - logp_orig[t]   (one fp32 subtraction)
 //     s     = |delta|,  eligible = mask[t] != 0 and delta finite.
-// The k largest s are found by a radix select on the bits of s (a
-// non-negative float orders like its bit pattern): four 8-bit digits, most
+// (In value mode, s is the value itself.)  Scores map to 32-bit keys that
+// order like the floats (sign-magnitude flipped to an unsigned order, -0
+// folded onto +0).  The k largest s are found by a radix select on the
+// keys: four 8-bit digits, most
 // significant first, each resolved from an LDS histogram.  That yields the
 // threshold score S and how many positions at exactly S are needed; those
 // are the lowest-indexed ties (a scan in position order).  The kk <= 1024
@@ -62,17 +66,30 @@ struct Pos {
   bool elig;
 };
 
+// Unsigned key ordered like the float (finite inputs); -0 maps like +0.
+__device__ __forceinline__ unsigned float_key(float f) {
+  const unsigned u = __float_as_uint(f == 0.f ? 0.f : f);
+  return (u & 0x80000000u) ? ~u : (u | 0x80000000u);
+}
+__device__ __forceinline__ float key_float(unsigned k) {
+  return __uint_as_float((k & 0x80000000u) ? (k & 0x7fffffffu) : ~k);
+}
+
+// VALUES: the score is lo[t] itself; otherwise |lh[t] - lo[t]| (one fp32
+// subtraction).
+template <bool VALUES>
 __device__ __forceinline__ Pos load_pos(const float* lo, const float* lh, const uint8_t* mask,
                                         int64_t base, int64_t t) {
   Pos p;
-  const float d = lh[base + t] - lo[base + t];
+  const float d = VALUES ? lo[base + t] : lh[base + t] - lo[base + t];
   const bool on = (mask == nullptr) || (mask[base + t] != 0);
   p.elig = on && __builtin_isfinite(d);
   p.delta = p.elig ? d : 0.f;
-  p.key = __float_as_uint(__builtin_fabsf(p.delta));
+  p.key = float_key(VALUES ? p.delta : __builtin_fabsf(p.delta));
   return p;
 }
 
+template <bool VALUES>
 __global__ __launch_bounds__(kThreads) void select_kernel(const float* __restrict__ lo,
                                                           const float* __restrict__ lh,
                                                           const uint8_t* __restrict__ mask,
@@ -89,7 +106,7 @@ __global__ __launch_bounds__(kThreads) void select_kernel(const float* __restric
   // ---- eligibility count (and the optional signed delta) -----------------
   int c = 0;
   for (int64_t t = tid; t < T; t += kThreads) {
-    const Pos p = load_pos(lo, lh, mask, base, t);
+    const Pos p = load_pos<VALUES>(lo, lh, mask, base, t);
     if (delta_out) delta_out[base + t] = p.delta;
     c += p.elig ? 1 : 0;
   }
@@ -105,7 +122,7 @@ __global__ __launch_bounds__(kThreads) void select_kernel(const float* __restric
       for (int i = tid; i < 256; i += kThreads) sh.hist[i] = 0;
       __syncthreads();
       for (int64_t t = tid; t < T; t += kThreads) {
-        const Pos p = load_pos(lo, lh, mask, base, t);
+        const Pos p = load_pos<VALUES>(lo, lh, mask, base, t);
         if (p.elig && (p.key & pmask) == prefix) atomicAdd(&sh.hist[(p.key >> shift) & 255], 1);
       }
       __syncthreads();
@@ -132,7 +149,7 @@ __global__ __launch_bounds__(kThreads) void select_kernel(const float* __restric
     for (int64_t t0 = 0; t0 < T; t0 += kThreads) {
       const int64_t t = t0 + tid;
       Pos p;
-      if (t < T) p = load_pos(lo, lh, mask, base, t);
+      if (t < T) p = load_pos<VALUES>(lo, lh, mask, base, t);
       else { p.elig = false; p.key = 0; p.delta = 0.f; }
       const bool eq = p.elig && p.key == thr;
       int n_eq;
@@ -149,6 +166,8 @@ __global__ __launch_bounds__(kThreads) void select_kernel(const float* __restric
     __syncthreads();
 
     // ---- bitonic sort, descending, of the kk winners ----------------------
+    // (padding keys are 0, below every real key: a finite score's key is at
+    // least 0x00800000, so every real composite key is positive)
     int P = 1;
     while (P < kk) P <<= 1;
     for (int i = kk + tid; i < P; i += kThreads) sh.keys[i] = 0ull;
@@ -175,7 +194,7 @@ __global__ __launch_bounds__(kThreads) void select_kernel(const float* __restric
     if (j < kk) {
       const unsigned long long key = sh.keys[j];
       idx[static_cast<int64_t>(r) * k + j] = static_cast<int32_t>(0xFFFFFFFFu - static_cast<unsigned>(key & 0xFFFFFFFFull));
-      score[static_cast<int64_t>(r) * k + j] = __uint_as_float(static_cast<unsigned>(key >> 32));
+      score[static_cast<int64_t>(r) * k + j] = key_float(static_cast<unsigned>(key >> 32));
     } else {
       idx[static_cast<int64_t>(r) * k + j] = -1;
       score[static_cast<int64_t>(r) * k + j] = 0.f;
@@ -188,9 +207,13 @@ __global__ __launch_bounds__(kThreads) void select_kernel(const float* __restric
 
 hipError_t launch_select(const float* lo, const float* lh, const uint8_t* mask, int64_t n_roots,
                          int64_t T, int k, int32_t* idx, float* score, int32_t* count, float* delta,
-                         hipStream_t stream) {
-  hipLaunchKernelGGL(select_kernel, dim3(static_cast<unsigned>(n_roots)), dim3(kThreads), 0, stream,
-                     lo, lh, mask, T, k, idx, score, count, delta);
+                         bool values, hipStream_t stream) {
+  if (values)
+    hipLaunchKernelGGL(select_kernel<true>, dim3(static_cast<unsigned>(n_roots)), dim3(kThreads), 0,
+                       stream, lo, lh, mask, T, k, idx, score, count, delta);
+  else
+    hipLaunchKernelGGL(select_kernel<false>, dim3(static_cast<unsigned>(n_roots)), dim3(kThreads), 0,
+                       stream, lo, lh, mask, T, k, idx, score, count, delta);
   return hipGetLastError();
 }
 

@@ -28,8 +28,9 @@ def lib():
 
 def test_header_declares_the_boundary():
     names = _declared_functions()
-    for n in ("hdl_token_logprobs", "hdl_select_branch_points", "hdl_token_logprobs_workspace_size",
-              "hdl_status_string", "hdl_last_error"):
+    for n in ("hdl_token_logprobs", "hdl_token_logprobs_entropy", "hdl_select_branch_points",
+              "hdl_select_top_k", "hdl_token_logprobs_workspace_size", "hdl_status_string",
+              "hdl_last_error"):
         assert n in names
 
 
@@ -42,7 +43,7 @@ def test_status_strings(lib):
     assert lib.hdl_status_string(0) == b"ok"
     for s in (-1, -2, -3, -4):
         assert lib.hdl_status_string(s) not in (b"ok", b"unknown status")
-    assert lib.hdl_abi_version() == 1
+    assert lib.hdl_abi_version() == 2
 
 
 def test_workspace_size_rules(lib):
@@ -77,3 +78,15 @@ def test_select_argument_errors(lib):
     assert call(p, p, None, 1, 10, 0, p, p, p, None, None) == -1
     assert call(p, p, None, 1, 10, 1025, p, p, p, None, None) == -2
     assert b"1025" in lib.hdl_last_error()
+
+
+def test_entropy_and_value_topk_argument_errors(lib):
+    p = ctypes.c_void_p(4096)
+    f = lib.hdl_token_logprobs_entropy
+    assert f(p, p, p, None, 4, 64, 10, 1, p, None, None, p, 1 << 20, None) == -1   # null entropy
+    assert f(None, p, p, None, 4, 64, 10, 1, p, None, p, p, 1 << 20, None) == -1
+    assert f(p, p, p, None, 4, 12, 10, 1, p, None, p, p, 1 << 20, None) == -2
+    g = lib.hdl_select_top_k
+    assert g(None, None, 1, 10, 2, p, p, p, None) == -1
+    assert g(p, None, 1, 10, 0, p, p, p, None) == -1
+    assert g(p, None, 1, 10, 1025, p, p, p, None) == -2

@@ -18,6 +18,7 @@ import numpy as np
 import pytest
 import torch
 
+import workloads
 from oracle import hdl_oracle as O
 
 GOLDEN = os.path.join(os.path.dirname(__file__), "golden", "hand_worked.json")
@@ -366,3 +367,59 @@ def test_entropy_closed_forms():
     Z = math.fsum(math.exp(v) for v in z)
     want = -math.fsum((math.exp(v) / Z) * math.log(math.exp(v) / Z) for v in z)
     assert abs(O.token_entropy(h3, W3)[0] - want) < 1e-12
+    # two words: the binary entropy of p = sigmoid(z0 - z1)
+    W4 = np.array([[1.5, 0.0], [0.0, 1.0]])
+    h4 = np.array([[0.8, -0.3]])
+    p = 1.0 / (1.0 + math.exp(-(1.5 * 0.8 + 0.3)))
+    assert abs(O.token_entropy(h4, W4)[0] - (-p * math.log(p) - (1 - p) * math.log(1 - p))) < 1e-14
+
+
+# ------------------------------------------------------- top-k over values
+def test_select_by_value_matches_rank_counting():
+    # position t is in the top-k iff fewer than k eligible positions beat it,
+    # where u beats t when v_u > v_t, or v_u == v_t and u < t (the ranking rule
+    # of Sec. 3.2 applied to an arbitrary value); negatives, +-0, +-inf, NaN
+    rng = np.random.default_rng(77)
+    for trial in range(40):
+        R, T, k = 3, int(rng.integers(1, 40)), int(rng.integers(1, 12))
+        v = rng.choice([-3.0, -1.0, -0.0, 0.0, 0.5, 2.0, np.inf, -np.inf, np.nan], size=(R, T))
+        fresh = rng.random((R, T)) < 0.5
+        v[fresh] = np.round(rng.normal(size=int(fresh.sum())), 1)   # rounding makes ties
+        mask = (rng.random((R, T)) < 0.8).astype(np.uint8)
+        idx, score, count = O.select_by_value(v, mask, k)
+        for r in range(R):
+            elig = [t for t in range(T) if mask[r, t] and np.isfinite(v[r, t])]
+            beats = {t: sum(1 for u in elig if v[r, u] > v[r, t] or (v[r, u] == v[r, t] and u < t))
+                     for t in elig}
+            want = sorted((t for t in elig if beats[t] < k), key=lambda t: beats[t])
+            assert count[r] == len(want) == min(k, len(elig))
+            assert idx[r, :count[r]].tolist() == want
+            assert np.all(idx[r, count[r]:] == -1) and np.all(score[r, count[r]:] == 0.0)
+            assert np.array_equal(score[r, :count[r]], v[r, want])
+
+
+def test_select_by_value_on_abs_difference_is_branch_selection():
+    # ranking |log p^H - log p^0| by value must reproduce the Eq. 2 selection
+    lo, lh, mask = workloads.make_logp_pair(4, 300, seed=5, nan_rows=2)
+    _, s, elig = O.divergence(lo, lh, mask)
+    vals = np.where(elig, s, np.nan)
+    a = O.select_by_value(vals, None, 9)
+    b = O.select_branch_points(lo, lh, mask, 9)
+    for x, y in zip(a, b):
+        assert np.array_equal(x, y)
+
+
+def test_entropy_is_lse_minus_expected_logit():
+    # H = lse - E_p[z]: the identity the fused kernel's third accumulator uses,
+    # checked against the definition -sum p log p on random rows
+    rng = np.random.default_rng(3)
+    W = rng.normal(size=(700, 16))
+    h = rng.normal(size=(5, 16)) * 2
+    z = h @ W.T
+    lse = np.log(np.exp(z - z.max(1, keepdims=True)).sum(1)) + z.max(1)
+    p = np.exp(z - lse[:, None])
+    assert np.allclose(O.token_entropy(h, W), lse - (p * z).sum(1), atol=1e-11)
+    # masked rows are 0; entropy never exceeds log V
+    m = np.array([1, 0, 1, 0, 1], np.uint8)
+    H = O.token_entropy(h, W, m)
+    assert np.all(H[m == 0] == 0.0) and np.all(H <= np.log(700) + 1e-12)
