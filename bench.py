@@ -31,6 +31,8 @@ PEAK_TFLOPS = {"bf16": 2500.0, "f32": 157.3}   # MI355X dense MFMA (fp32: matrix
 METRIC = "scored tokens/sec (both contexts) + MFMA util of fused lm-head logprob kernel"
 # The Entropy localization baseline (Sec. 4.1) scores the original context only.
 METRIC_ENTROPY = "scored tokens/sec (original context) of fused lm-head entropy + top-k (Entropy baseline)"
+# Training side: gradients of the token-level policy loss (Sec. 3.3) through the lm-head.
+METRIC_BACKWARD = "trained tokens/sec of the lm-head backward (dL/dh, dL/dW) + MFMA util"
 
 
 def log(msg: str) -> None:
@@ -126,6 +128,9 @@ def main() -> int:
     ap.add_argument("--selector", default="hdl", choices=["hdl", "entropy"],
                     help="hdl: both contexts, |delta log p| top-k (default); entropy: the Entropy "
                          "baseline, next-token entropy of the original context and its top-k")
+    ap.add_argument("--backward", action="store_true",
+                    help="time the backward pass (gradients with respect to the hidden states and the "
+                         "lm-head weight) on the original-context rows instead of the re-scoring step")
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--cpu-budget", type=float, default=15.0)
     ap.add_argument("--no-mfma-ceiling", action="store_true",
@@ -156,6 +161,9 @@ def main() -> int:
     w = workloads.make_workload(args.workload)
     c = w.cfg
     log(f"generated workload {args.workload} in {time.time() - t0:.1f} s")
+
+    if args.backward:
+        return bench_backward(args, w, hdl, dev)
 
     ent_sel = args.selector == "entropy"
     n_keep = c.R * c.T if ent_sel else 2 * c.R * c.T   # rows are [context][root][t]
@@ -261,6 +269,121 @@ def main() -> int:
         result["cpu_baseline"] = cpu_baseline(w, budget_s=args.cpu_budget, entropy=ent_sel)
     print(json.dumps(result), flush=True)
     return 0
+
+
+def cpu_baseline_backward(w, budget_s: float = 15.0, max_rows: int = 2048):
+    """Time the float64 oracle's backward on a seeded sample of eligible
+    original-context rows; return oracle trained tokens/s."""
+    import numpy as np
+    import torch
+    from oracle import hdl_oracle as O
+    try:
+        from threadpoolctl import threadpool_info
+        cores = max([int(i.get("num_threads", 1)) for i in threadpool_info() if i.get("user_api") == "blas"] or [1])
+    except Exception:  # pragma: no cover - informational only
+        cores = os.cpu_count() or 1
+    c = w.cfg
+    Wd = O.bf16_bits_to_f64(w.W.view(torch.int16).numpy().view(np.uint16))
+    n0 = c.R * c.T
+    hidden = w.rows_hidden()[:n0]
+    tokens = w.rows_tokens().numpy()[:n0]
+    elig = np.nonzero(w.rows_mask().numpy()[:n0])[0]
+    rng = np.random.default_rng(12346)
+    sample = rng.permutation(elig)[:max_rows]
+    done, t_total, blk = 0, 0.0, 32
+    while done < len(sample) and t_total < budget_s:
+        rows = np.sort(sample[done:done + blk])
+        H = O.bf16_bits_to_f64(hidden[torch.as_tensor(rows)].view(torch.int16).numpy().view(np.uint16))
+        g = rng.normal(size=len(rows))
+        t0 = time.perf_counter()
+        O.token_logprobs_backward(H, Wd, tokens[rows], g)
+        t_total += time.perf_counter() - t0
+        done += len(rows)
+    return {"value": done / t_total, "unit": "trained tokens/s", "cores": cores, "kind": "oracle",
+            "sample": f"{done} eligible original-context rows of this workload (float64 logits, "
+                      f"softmax gradient, dL/dh and dL/dW, {t_total:.1f} s)"}
+
+
+def bench_backward(args, w, hdl, dev) -> int:
+    """Backward pass of the fused log-probability on the original-context rows:
+    the logits are recomputed tile by tile, the logit gradient exists one chunk
+    at a time as bf16, and dL/dh = G W and dL/dW = G^T H run as MFMA GEMMs."""
+    import numpy as np
+    import torch
+    c = w.cfg
+    if c.dtype != "bf16":
+        print("the backward pass takes bf16 inputs", file=sys.stderr)
+        return 2
+    n0 = c.R * c.T
+    hidden = w.rows_hidden()[:n0].to(dev)
+    W = w.W.to(dev)
+    tokens = w.rows_tokens()[:n0].to(dev)
+    mask = w.rows_mask()[:n0].to(dev)
+    n_scored = int(mask.sum().item())
+    # per-token factor of a token-level policy loss: advantage-like, averaged over tokens
+    g = torch.from_numpy(np.random.default_rng(c.seed + 7).normal(size=n0).astype(np.float32) / n_scored).to(dev)
+    _, lse = hdl.token_logprobs(hidden, W, tokens, mask)
+    ws = torch.empty(hdl.backward_workspace_size(n0, c.d, c.V), dtype=torch.uint8, device=dev)
+    grad_w = torch.empty(c.V, c.d, dtype=torch.float32, device=dev)
+    torch.cuda.synchronize()
+    log(f"backward: {n0} rows, {n_scored} trained, workspace {ws.numel() / 2**30:.2f} GiB")
+
+    def step():
+        return hdl.token_logprobs_backward(hidden, W, tokens, mask, lse, g, grad_w=grad_w, workspace=ws)
+
+    for _ in range(args.warmup):
+        step()
+    torch.cuda.synchronize()
+    stream = torch.cuda.current_stream(dev)
+    ev0 = torch.cuda.Event(enable_timing=True)
+    ev1 = torch.cuda.Event(enable_timing=True)
+    torch.cuda.synchronize()
+    ev0.record(stream)
+    for _ in range(args.steps):
+        dh, dw = step()
+    ev1.record(stream)
+    torch.cuda.synchronize()
+    step_ms = ev0.elapsed_time(ev1) / args.steps
+    log(f"timed {args.steps} backward steps: {step_ms:.3f} ms/step")
+    if not (torch.isfinite(dh).all() and torch.isfinite(dw).all()):
+        raise RuntimeError("non-finite gradients")
+    # probabilities sum to one, so the vocabulary rows of dL/dW sum to ~0
+    col = dw.double().sum(0).abs().max().item()
+    log(f"max |sum_v dL/dW[v, :]| = {col:.3g} (max |dL/dW| = {dw.abs().max().item():.3g})")
+    flops = 6.0 * c.d * c.V * n_scored   # logit recompute + two contractions
+    achieved = flops / (step_ms / 1e3) / 1e12
+    peak = PEAK_TFLOPS[c.dtype]
+    result = {
+        "metric": METRIC_BACKWARD,
+        "value": n_scored / (step_ms / 1e3),
+        "unit": "trained tokens/s",
+        "n_gpus": 1,
+        "steps": args.steps,
+        "warmup": args.warmup,
+        "ms_per_step": step_ms,
+        "higher_is_better": True,
+        "scaling": "weak",
+        "vs_baseline": None,
+        "dtype": c.dtype,
+        "data": "synthetic (seeded generator; random lm-head weights, hidden states and upstream gradients)",
+        "config": {"workload": f"{args.workload}: {workloads_description(args.workload)}, original context",
+                   "pass": "backward", "roots": c.R, "T": c.T, "d": c.d, "V": c.V,
+                   "trained_tokens_per_step": n_scored},
+        "roofline": {"bound": "mfma", "achieved": achieved, "peak": peak, "unit": "TFLOP/s",
+                     "frac": achieved / peak, "traffic": None,
+                     "kernel": "whole backward pass (gradient-mode lm-head kernel + 2 GEMMs + transposes)",
+                     "kernel_ms": step_ms, "flops_per_launch": flops},
+    }
+    if not args.no_cpu_baseline:
+        log("timing the float64 oracle backward on a bounded sample")
+        result["cpu_baseline"] = cpu_baseline_backward(w, budget_s=args.cpu_budget)
+    print(json.dumps(result), flush=True)
+    return 0
+
+
+def workloads_description(name: str) -> str:
+    import workloads
+    return workloads.DESCRIPTIONS[name]
 
 
 if __name__ == "__main__":

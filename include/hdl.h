@@ -155,6 +155,49 @@ int hdl_select_branch_points(const float* logp_orig, const float* logp_hind,
 int hdl_select_top_k(const float* values, const uint8_t* mask, int64_t n_roots, int64_t T,
                      int32_t k, int32_t* idx, float* score, int32_t* count, void* stream);
 
+/*
+ * Bytes of device workspace hdl_token_logprobs_backward needs for these sizes
+ * (0 if the sizes are invalid or unsupported).  Dominated by two copies of
+ * one chunk's logit gradient: 4 * min(n_rows, 8192) * round_up(vocab, 64)
+ * bytes (C2 shapes: 5 GB), plus round_up(vocab, 64) * d * 2 bytes for the
+ * transposed weight.
+ */
+size_t hdl_token_logprobs_backward_workspace_size(int64_t n_rows, int64_t d, int64_t vocab,
+                                                  int dtype);
+
+/*
+ * Backward pass of hdl_token_logprobs for a loss L = sum_n g_n log p_n(y_n)
+ * (the policy loss of Sec. 3.3 is such a sum over the tokens it trains on;
+ * g_n is its derivative with respect to each token's log-likelihood):
+ *
+ *     G[n][v]  = g_n (1[v == y_n] - p_n(v))          (dL/dz, never stored whole)
+ *     dL/dh_n  = sum_v G[n][v] W[v]                  -> grad_hidden
+ *     dL/dW_v  = sum_n G[n][v] h_n                   -> grad_w
+ *
+ * The logits are recomputed tile by tile from hidden and w_vocab; G exists
+ * only for one chunk of at most 8192 scored rows at a time, as bf16; the two
+ * contractions run on bf16 MFMA tiles with fp32 accumulation.
+ *
+ *  hidden, w_vocab, tokens, mask, n_rows, d, vocab: as for hdl_token_logprobs;
+ *               dtype must be HDL_BF16.  Hidden states must not exceed 4 GiB.
+ *  lse          [n_rows] fp32: the log-sum-exp hdl_token_logprobs returned
+ *               for the same inputs (read for scored rows only).
+ *  grad_logp    [n_rows] fp32: g_n (read for scored rows only).
+ *  grad_hidden  [n_rows, d] fp32 out; rows with mask == 0 are set to 0.
+ *  grad_w       [vocab, d] fp32 out; overwritten, or accumulated into when
+ *               accumulate_w != 0.
+ *  workspace    hdl_token_logprobs_backward_workspace_size(...) bytes,
+ *               256-byte aligned.
+ *
+ * A token outside [0, vocab) contributes no indicator term (G = -g p).
+ * Deterministic: fixed chunking and fixed-order sums, no atomics.
+ */
+int hdl_token_logprobs_backward(const void* hidden, const void* w_vocab, const int32_t* tokens,
+                                const uint8_t* mask, const float* lse, const float* grad_logp,
+                                int64_t n_rows, int64_t d, int64_t vocab, int dtype,
+                                float* grad_hidden, float* grad_w, int accumulate_w,
+                                void* workspace, size_t workspace_bytes, void* stream);
+
 /* Static description of a status code. */
 const char* hdl_status_string(int status);
 

@@ -32,6 +32,13 @@ Readings where the paper is silent (each also listed in the design notes):
   a candidate;
 * fewer than k candidates: count < k, idx padded with -1, score with 0.0.
 
+Backward (training side, Sec. 3.3: roots and continuations are trained with
+the same token-level policy loss): for L = sum_n g_n log p_n(y_n), where g_n
+is whatever the loss puts on each token's log-likelihood, the gradients with
+respect to the final hidden states and the lm-head weight follow from
+d log p_n(y) / d z_n[v] = 1[v == y] - p_n(v).  Masked rows contribute
+nothing and get a zero gradient; a token outside [0, V) has no indicator term.
+
 Pins: every function here is checked by tests that do not re-type its formula
 (brute-force softmax with exact summation, closed forms, invariants, hand-worked
 fixtures, brute-force sorting).  See tests/test_oracle_pins.py.
@@ -121,6 +128,36 @@ def token_entropy(hidden: np.ndarray, W: np.ndarray,
         logq = z - (m + np.log(np.exp(z - m).sum(axis=1, keepdims=True)))
         out[r] = -(np.exp(logq) * logq).sum(axis=1)
     return out
+
+
+def token_logprobs_backward(hidden: np.ndarray, W: np.ndarray, tokens: np.ndarray,
+                            grad_logp: np.ndarray, mask: Optional[np.ndarray] = None):
+    """Gradients of L = sum_n g_n log p_n(tokens[n]) (Eq. 1's log-likelihood,
+    weighted by the policy loss's per-token factor g_n, Sec. 3.3).
+
+    With G[n, v] = g_n (1[v == y_n] - p_n(v)):
+        dL/dhidden = G W        [N, d]
+        dL/dW      = G^T hidden [V, d]
+    Also returns the element-wise magnitudes sum_v |G| |W| and sum_n |G| |h|,
+    which bound how far a result computed from a rounded G can move.
+    Returns (dH, dW, mag_dH, mag_dW), all float64; masked rows of dH are 0.
+    """
+    H = np.asarray(hidden, dtype=np.float64)
+    W = np.asarray(W, dtype=np.float64)
+    y = np.asarray(tokens).astype(np.int64)
+    g = np.asarray(grad_logp, dtype=np.float64)
+    N, V = H.shape[0], W.shape[0]
+    keep = np.ones(N, bool) if mask is None else (np.asarray(mask) != 0)
+    z = H @ W.T
+    m = z.max(axis=1, keepdims=True)
+    P = np.exp(z - m)
+    P /= P.sum(axis=1, keepdims=True)
+    onehot = np.zeros((N, V))
+    ok = (y >= 0) & (y < V)
+    onehot[np.nonzero(ok)[0], y[ok]] = 1.0
+    G = g[:, None] * (onehot - P)
+    G[~keep] = 0.0
+    return G @ W, G.T @ H, np.abs(G) @ np.abs(W), np.abs(G).T @ np.abs(H)
 
 
 # ---------------------------------------------------------------------------

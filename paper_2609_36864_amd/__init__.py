@@ -18,7 +18,8 @@ from typing import Optional, Tuple
 import torch
 
 __all__ = ["HdlError", "HDL_F32", "HDL_BF16", "HDL_MAX_K", "library_path", "load_library",
-           "workspace_size", "token_logprobs", "select_branch_points", "select_top_k", "rescore",
+           "workspace_size", "token_logprobs", "token_logprobs_backward", "select_branch_points",
+           "select_top_k", "rescore",
            "profile_enable", "profile_read", "abi_version"]
 
 HDL_F32 = 0
@@ -59,6 +60,11 @@ def load_library() -> ctypes.CDLL:
     L.hdl_token_logprobs_entropy.restype = ctypes.c_int
     L.hdl_select_top_k.argtypes = [c_vp, c_vp, c_i64, c_i64, ctypes.c_int32, c_vp, c_vp, c_vp, c_vp]
     L.hdl_select_top_k.restype = ctypes.c_int
+    L.hdl_token_logprobs_backward_workspace_size.argtypes = [c_i64, c_i64, c_i64, ctypes.c_int]
+    L.hdl_token_logprobs_backward_workspace_size.restype = c_sz
+    L.hdl_token_logprobs_backward.argtypes = [c_vp, c_vp, c_vp, c_vp, c_vp, c_vp, c_i64, c_i64, c_i64,
+                                              ctypes.c_int, c_vp, c_vp, ctypes.c_int, c_vp, c_sz, c_vp]
+    L.hdl_token_logprobs_backward.restype = ctypes.c_int
     L.hdl_select_branch_points.argtypes = [c_vp, c_vp, c_vp, c_i64, c_i64, ctypes.c_int32,
                                            c_vp, c_vp, c_vp, c_vp, c_vp]
     L.hdl_select_branch_points.restype = ctypes.c_int
@@ -228,6 +234,62 @@ def select_top_k(values: torch.Tensor, mask: Optional[torch.Tensor], k: int):
     _check(L.hdl_select_top_k(values.data_ptr(), _ptr(mask), R, T, int(k), idx.data_ptr(),
                               score.data_ptr(), count.data_ptr(), _stream_handle(dev)))
     return idx, score, count
+
+
+def token_logprobs_backward(hidden: torch.Tensor, w_vocab: torch.Tensor, tokens: torch.Tensor,
+                            mask: Optional[torch.Tensor], lse: torch.Tensor, grad_logp: torch.Tensor, *,
+                            grad_w: Optional[torch.Tensor] = None, accumulate_w: bool = False,
+                            workspace: Optional[torch.Tensor] = None):
+    """Gradients of L = sum_n g_n log p_n(y_n) with respect to the hidden
+    states and the lm-head weight (backward of token_logprobs; bf16 inputs).
+
+    lse is the forward pass's log-sum-exp, grad_logp the per-row g_n (fp32).
+    Returns (grad_hidden [n_rows, d] fp32, grad_w [vocab, d] fp32).
+    """
+    L = load_library()
+    for name, t in (("hidden", hidden), ("w_vocab", w_vocab), ("tokens", tokens), ("lse", lse),
+                    ("grad_logp", grad_logp)):
+        _require_cuda(name, t)
+    if hidden.dim() != 2 or w_vocab.dim() != 2 or hidden.shape[1] != w_vocab.shape[1]:
+        raise ValueError("hidden must be [n_rows, d] and w_vocab [vocab, d]")
+    if hidden.dtype != torch.bfloat16 or w_vocab.dtype != torch.bfloat16:
+        raise ValueError("the backward pass takes bfloat16 hidden and w_vocab")
+    n_rows, d = hidden.shape
+    vocab = w_vocab.shape[0]
+    if tokens.dtype != torch.int32 or tokens.shape != (n_rows,):
+        raise ValueError("tokens must be int32 [n_rows]")
+    for name, t in (("lse", lse), ("grad_logp", grad_logp)):
+        if t.dtype != torch.float32 or t.shape != (n_rows,):
+            raise ValueError(f"{name} must be float32 [n_rows]")
+    dev = hidden.device
+    if mask is not None:
+        _require_cuda("mask", mask)
+        if mask.dtype == torch.bool:
+            mask = mask.view(torch.uint8)
+        if mask.dtype != torch.uint8 or mask.shape != (n_rows,):
+            raise ValueError("mask must be uint8 [n_rows]")
+    grad_hidden = torch.empty(n_rows, d, dtype=torch.float32, device=dev)
+    if grad_w is None:
+        if accumulate_w:
+            raise ValueError("accumulate_w needs grad_w")
+        grad_w = torch.empty(vocab, d, dtype=torch.float32, device=dev)
+    else:
+        _require_cuda("grad_w", grad_w)
+        if grad_w.dtype != torch.float32 or grad_w.shape != (vocab, d):
+            raise ValueError("grad_w must be float32 [vocab, d]")
+    nbytes = int(L.hdl_token_logprobs_backward_workspace_size(n_rows, d, vocab, HDL_BF16))
+    if nbytes == 0:
+        raise ValueError(f"unsupported sizes n_rows={n_rows} d={d} vocab={vocab}")
+    ws = workspace if workspace is not None else torch.empty(nbytes, dtype=torch.uint8, device=dev)
+    _check(L.hdl_token_logprobs_backward(hidden.data_ptr(), w_vocab.data_ptr(), tokens.data_ptr(), _ptr(mask),
+                                         lse.data_ptr(), grad_logp.data_ptr(), n_rows, d, vocab, HDL_BF16,
+                                         grad_hidden.data_ptr(), grad_w.data_ptr(), 1 if accumulate_w else 0,
+                                         ws.data_ptr(), ws.numel() * ws.element_size(), _stream_handle(dev)))
+    return grad_hidden, grad_w
+
+
+def backward_workspace_size(n_rows: int, d: int, vocab: int) -> int:
+    return int(load_library().hdl_token_logprobs_backward_workspace_size(n_rows, d, vocab, HDL_BF16))
 
 
 def rescore(hidden_both: torch.Tensor, w_vocab: torch.Tensor, tokens: torch.Tensor,

@@ -96,7 +96,7 @@ __global__ __launch_bounds__(kThreads) void scatter_kernel(const uint8_t* __rest
     if (on[i]) {
       rows[pos++] = static_cast<int32_t>(n);
     } else {
-      logp[n] = 0.f;
+      if (logp) logp[n] = 0.f;
       if (lse) lse[n] = 0.f;
       if (entropy) entropy[n] = 0.f;
     }

@@ -167,6 +167,8 @@ int token_stats(const char* fn, const void* hidden, const void* w_vocab, const i
     a.part_s = part + plane;
     a.part_z = part + 2 * plane;
     a.part_t = entropy ? part + 3 * plane : nullptr;
+    a.row_base = 0;
+    a.row_cap = n;
 
     std::pair<hipEvent_t, hipEvent_t> ev{nullptr, nullptr};
     bool timed = false;
@@ -270,7 +272,7 @@ const char* hdl_status_string(int status) {
 
 const char* hdl_last_error(void) { return g_last_error; }
 
-int hdl_abi_version(void) { return 2; }
+int hdl_abi_version(void) { return 3; }
 
 int hdl_profile_enable(int on) {
   std::lock_guard<std::mutex> lk(g_prof.mu);
@@ -295,6 +297,211 @@ int hdl_profile_read(double* total_ms, int64_t* launches) {
   g_prof.pending.clear();
   if (total_ms) *total_ms = tot;
   if (launches) *launches = n;
+  return HDL_OK;
+}
+
+}  // extern "C"
+
+// ---- backward pass --------------------------------------------------------
+namespace {
+
+// How one hdl_token_logprobs_backward call is cut up.  Scored rows are taken
+// in chunks of `nc`; for each chunk the gradient with respect to the logits
+// G [nc][v_pad] (bf16) and its transpose exist at once, never more.
+struct BwdPlan {
+  int64_t nc, v_pad, n_chunks;
+  int64_t splits, k_split;      // vocabulary split of the dH contraction
+  hdl::LmheadPlan fwd;          // gradient-mode lm-head launches (nc rows)
+  size_t off_rows, off_count, off_wt, off_g, off_gt, off_ht, off_hpart, bytes;
+};
+
+constexpr int64_t kBwdChunkRows = 8192;
+
+BwdPlan make_bwd_plan(int64_t n_rows, int64_t vocab, int64_t d) {
+  BwdPlan p{};
+  p.nc = n_rows < kBwdChunkRows ? static_cast<int64_t>(round_up(static_cast<size_t>(n_rows), 256))
+                                : kBwdChunkRows;
+  p.v_pad = static_cast<int64_t>(round_up(static_cast<size_t>(vocab), 64));
+  p.n_chunks = (n_rows + p.nc - 1) / p.nc;
+  // dH = G W has nc/256 x d/256 output tiles; split the vocabulary so that
+  // about 512 workgroups run.
+  const int64_t tiles = (p.nc / hdl::kTileN) * ((d + hdl::kTileN - 1) / hdl::kTileN);
+  int64_t s = (512 + tiles - 1) / tiles;
+  s = s < 1 ? 1 : (s > 8 ? 8 : s);
+  const int64_t slices = p.v_pad / 64;
+  if (s > slices) s = slices;
+  p.k_split = (slices + s - 1) / s * 64;
+  p.splits = (p.v_pad + p.k_split - 1) / p.k_split;
+  p.fwd = hdl::make_plan(p.nc, vocab, d, 2);
+  size_t off = 0;
+  p.off_rows = off;
+  off = round_up(off + sizeof(int32_t) * static_cast<size_t>(n_rows), 256);
+  p.off_count = off;
+  off = round_up(off + sizeof(int32_t) * (64 + static_cast<size_t>((n_rows + 4095) / 4096)), 256);
+  p.off_wt = off;   // W^T [d][v_pad] bf16
+  off = round_up(off + 2 * static_cast<size_t>(d) * static_cast<size_t>(p.v_pad), 256);
+  p.off_g = off;    // G [nc][v_pad] bf16
+  off = round_up(off + 2 * static_cast<size_t>(p.nc) * static_cast<size_t>(p.v_pad), 256);
+  p.off_gt = off;   // G^T [v_pad][nc] bf16
+  off = round_up(off + 2 * static_cast<size_t>(p.nc) * static_cast<size_t>(p.v_pad), 256);
+  p.off_ht = off;   // chunk hidden rows transposed [d][nc] bf16
+  off = round_up(off + 2 * static_cast<size_t>(d) * static_cast<size_t>(p.nc), 256);
+  p.off_hpart = off;   // dH partial sums [splits][nc][d] fp32
+  off = round_up(off + 4 * static_cast<size_t>(p.splits) * static_cast<size_t>(p.nc) * static_cast<size_t>(d), 256);
+  p.bytes = off;
+  return p;
+}
+
+hdl::GemmArgs gemm_args(const void* a, int64_t lda, const void* b, int64_t ldb, int64_t m, int64_t n, int64_t k,
+                        float* c, int64_t ldc) {
+  hdl::GemmArgs g{};
+  g.a = a;
+  g.lda = lda;
+  g.b = b;
+  g.ldb = ldb;
+  g.m = m;
+  g.n = n;
+  g.k = k;
+  g.k_split = k;
+  g.splits = 1;
+  g.tiles_m = (m + hdl::kTileV - 1) / hdl::kTileV;
+  g.tiles_n = (n + hdl::kTileN - 1) / hdl::kTileN;
+  g.gn = g.tiles_n < 4 ? g.tiles_n : 4;
+  g.gm = 32 / g.gn;
+  g.c = c;
+  g.ldc = ldc;
+  return g;
+}
+
+}  // namespace
+
+extern "C" {
+
+size_t hdl_token_logprobs_backward_workspace_size(int64_t n_rows, int64_t d, int64_t vocab, int dtype) {
+  if (n_rows <= 0 || d <= 0 || vocab <= 0 || n_rows > INT32_MAX || vocab > INT32_MAX) return 0;
+  if (dtype != HDL_BF16 || d % 8 != 0) return 0;
+  if (hdl::rows_per_launch(d, 2) < n_rows) return 0;
+  return make_bwd_plan(n_rows, vocab, d).bytes;
+}
+
+int hdl_token_logprobs_backward(const void* hidden, const void* w_vocab, const int32_t* tokens,
+                                const uint8_t* mask, const float* lse, const float* grad_logp,
+                                int64_t n_rows, int64_t d, int64_t vocab, int dtype, float* grad_hidden,
+                                float* grad_w, int accumulate_w, void* workspace, size_t workspace_bytes,
+                                void* stream) {
+  const char* fn = "hdl_token_logprobs_backward";
+  if (!hidden || !w_vocab || !tokens || !lse || !grad_logp || !grad_hidden || !grad_w)
+    return fail(HDL_ERR_INVALID_ARG, "%s: null required pointer", fn);
+  if (n_rows <= 0 || d <= 0 || vocab <= 0)
+    return fail(HDL_ERR_INVALID_ARG, "%s: sizes must be positive (n_rows=%lld d=%lld vocab=%lld)", fn,
+                static_cast<long long>(n_rows), static_cast<long long>(d), static_cast<long long>(vocab));
+  if (n_rows > INT32_MAX || vocab > INT32_MAX)
+    return fail(HDL_ERR_UNSUPPORTED, "%s: n_rows and vocab must fit in int32", fn);
+  if (dtype != HDL_BF16) return fail(HDL_ERR_UNSUPPORTED, "%s: only bf16 inputs are supported", fn);
+  if (d % 8 != 0)
+    return fail(HDL_ERR_UNSUPPORTED, "%s: d=%lld is not a multiple of 8", fn, static_cast<long long>(d));
+  if (hdl::rows_per_launch(d, 2) < n_rows)
+    return fail(HDL_ERR_UNSUPPORTED, "%s: hidden states larger than 4 GiB", fn);
+  if (!aligned(hidden, 16) || !aligned(w_vocab, 16) || !aligned(grad_hidden, 16) || !aligned(grad_w, 16))
+    return fail(HDL_ERR_INVALID_ARG, "%s: hidden, w_vocab, grad_hidden and grad_w must be 16-byte aligned", fn);
+  const BwdPlan plan = make_bwd_plan(n_rows, vocab, d);
+  if (!workspace || workspace_bytes < plan.bytes)
+    return fail(HDL_ERR_WORKSPACE, "%s: workspace of %zu bytes needed, %zu given", fn, plan.bytes,
+                workspace ? workspace_bytes : static_cast<size_t>(0));
+  if (!aligned(workspace, 256)) return fail(HDL_ERR_INVALID_ARG, "%s: workspace must be 256-byte aligned", fn);
+  if (plan.fwd.grid > INT32_MAX) return fail(HDL_ERR_UNSUPPORTED, "%s: problem too large for one launch", fn);
+
+  hipStream_t s = static_cast<hipStream_t>(stream);
+  char* ws = static_cast<char*>(workspace);
+  int32_t* rows = reinterpret_cast<int32_t*>(ws + plan.off_rows);
+  int32_t* n_scored = reinterpret_cast<int32_t*>(ws + plan.off_count);
+  uint16_t* wt = reinterpret_cast<uint16_t*>(ws + plan.off_wt);
+  uint16_t* g = reinterpret_cast<uint16_t*>(ws + plan.off_g);
+  uint16_t* gt = reinterpret_cast<uint16_t*>(ws + plan.off_gt);
+  uint16_t* ht = reinterpret_cast<uint16_t*>(ws + plan.off_ht);
+  float* hpart = reinterpret_cast<float*>(ws + plan.off_hpart);
+
+  hipError_t e = hdl::launch_compact(mask, n_rows, rows, n_scored, nullptr, nullptr, nullptr, s);
+  if (e != hipSuccess) return hip_fail(e, "compaction launch");
+  if ((e = hdl::launch_zero_masked_rows(mask, n_rows, d, grad_hidden, s)) != hipSuccess)
+    return hip_fail(e, "row clearing launch");
+  hdl::TransposeArgs tw{};
+  tw.in = static_cast<const uint16_t*>(w_vocab);
+  tw.ld_in = d;
+  tw.r_cap = vocab;
+  tw.c_valid = d;
+  tw.out = wt;
+  tw.ld_out = plan.v_pad;
+  tw.out_rows = d;
+  if ((e = hdl::launch_transpose(tw, s)) != hipSuccess) return hip_fail(e, "transpose launch");
+
+  for (int64_t c = 0; c < plan.n_chunks; ++c) {
+    const int64_t base = c * plan.nc;
+    // 1. G for this chunk's scored rows (logits recomputed tile by tile)
+    hdl::LmheadArgs a{};
+    a.hidden = hidden;
+    a.w = w_vocab;
+    a.tokens = tokens;
+    a.rows = rows + base;
+    a.n_scored = n_scored;
+    a.d = d;
+    a.vocab = vocab;
+    a.n_vt = plan.fwd.n_vt;
+    a.tpc = plan.fwd.tpc;
+    a.n_ch = plan.fwd.n_ch;
+    a.n_grt = plan.fwd.n_grt;
+    a.row_base = base;
+    a.row_cap = plan.nc;
+    a.lse_in = lse;
+    a.grad_in = grad_logp;
+    a.g_out = g;
+    a.g_ld = plan.v_pad;
+    a.g_cols = plan.v_pad;
+    if ((e = hdl::launch_lmhead_grad(a, plan.fwd.grid, s)) != hipSuccess) return hip_fail(e, "gradient kernel launch");
+    // 2. G^T and the chunk's hidden rows transposed, zero beyond the scored rows
+    hdl::TransposeArgs tg{};
+    tg.in = g;
+    tg.ld_in = plan.v_pad;
+    tg.dyn = n_scored;
+    tg.dyn_base = base;
+    tg.r_cap = plan.nc;
+    tg.c_valid = plan.v_pad;
+    tg.out = gt;
+    tg.ld_out = plan.nc;
+    tg.out_rows = plan.v_pad;
+    if ((e = hdl::launch_transpose(tg, s)) != hipSuccess) return hip_fail(e, "transpose launch");
+    hdl::TransposeArgs th{};
+    th.in = static_cast<const uint16_t*>(hidden);
+    th.ld_in = d;
+    th.map = rows + base;
+    th.dyn = n_scored;
+    th.dyn_base = base;
+    th.r_cap = plan.nc;
+    th.c_valid = d;
+    th.out = ht;
+    th.ld_out = plan.nc;
+    th.out_rows = d;
+    if ((e = hdl::launch_transpose(th, s)) != hipSuccess) return hip_fail(e, "transpose launch");
+    // 3. dH rows of the chunk: G W, split along the vocabulary, partials summed in order
+    hdl::GemmArgs gh = gemm_args(g, plan.v_pad, wt, plan.v_pad, plan.nc, d, plan.v_pad, hpart, d);
+    gh.dyn = n_scored;
+    gh.dyn_base = base;
+    gh.dyn_dim = 1;
+    gh.k_split = plan.k_split;
+    gh.splits = plan.splits;
+    gh.c_split_stride = plan.nc * d;
+    if ((e = hdl::launch_gemm_nt(gh, s)) != hipSuccess) return hip_fail(e, "GEMM launch");
+    if ((e = hdl::launch_splitk_scatter(hpart, plan.splits, plan.nc * d, d, rows + base, n_scored, base, plan.nc,
+                                        grad_hidden, s)) != hipSuccess)
+      return hip_fail(e, "split-K sum launch");
+    // 4. dW (+)= G^T H over the chunk's rows
+    hdl::GemmArgs gw = gemm_args(gt, plan.nc, ht, plan.nc, vocab, d, plan.nc, grad_w, d);
+    gw.dyn = n_scored;
+    gw.dyn_base = base;
+    gw.dyn_dim = 2;
+    gw.beta = (c > 0 || accumulate_w) ? 1 : 0;
+    if ((e = hdl::launch_gemm_nt(gw, s)) != hipSuccess) return hip_fail(e, "GEMM launch");
+  }
   return HDL_OK;
 }
 

@@ -52,13 +52,69 @@ struct LmheadArgs {
   float* part_m;            // running max (natural-log units)
   float* part_s;            // sum of exp(z - m)
   float* part_z;            // sampled-token logit, -inf where not captured
-  float* part_t;            // sum of exp(z - m) * z, or nullptr (no entropy)
+  float* part_t;            // sum of exp(z - m) * (z - m), or nullptr (no entropy)
+  // Scored rows handled by this launch: rows[0 .. n) with
+  // n = clamp(*n_scored - row_base, 0, row_cap) (`rows` already offset).
+  int64_t row_base, row_cap;
+  // Gradient mode (backward pass): instead of partial statistics, write
+  // G[e][v] = g_e (1[v == y_e] - exp(z_ev - lse_e)) as bf16 for scored row e
+  // of this launch, columns v < g_cols (zero for v >= vocab).
+  const float* lse_in;      // [n_rows] log-sum-exp from the forward pass
+  const float* grad_in;     // [n_rows] upstream gradient of log p
+  uint16_t* g_out;          // [row_cap][g_ld] bf16, or nullptr (statistics mode)
+  int64_t g_ld, g_cols;
+};
+
+// Plain bf16 NT GEMM on the same 256 x 256 MFMA tile:
+//   C[s][m][n] (=|+=) sum_{k in split s} A[m][k] B[n][k]
+// A [M][lda] and B [N][ldb] are K-contiguous; K ranges are multiples of 64.
+struct GemmArgs {
+  const void* a;
+  int64_t lda;
+  const void* b;
+  int64_t ldb;
+  int64_t m, n, k;          // sizes (upper bounds when a dimension is dynamic)
+  // Dynamic dimension: dyn_dim 1 makes M = clamp(*dyn - dyn_base, 0, m);
+  // dyn_dim 2 makes K = round_up(clamp(*dyn - dyn_base, 0, k), 64).
+  const int32_t* dyn;
+  int64_t dyn_base;
+  int dyn_dim;
+  int64_t k_split;          // K elements per split (multiple of 64)
+  int64_t tiles_m, tiles_n, splits, gm, gn;   // launch grouping (host-computed)
+  float* c;
+  int64_t ldc, c_split_stride;
+  int beta;                 // 0: store, 1: accumulate
+};
+
+// Transpose of a bf16 matrix with zero fill and an optional row gather:
+//   out[c][r] = (r < r_valid && c < c_valid) ? in[map ? map[r] : r][c] : 0
+// for c < out_rows and r < r_cols_written, where r_valid is
+// clamp(*dyn - dyn_base, 0, r_cap) when dyn is given (else r_cap) and only
+// columns r < round_up(r_valid, 64) are written.  c_valid % 8 == 0.
+struct TransposeArgs {
+  const uint16_t* in;
+  int64_t ld_in;
+  const int32_t* map;
+  const int32_t* dyn;
+  int64_t dyn_base, r_cap, c_valid;
+  uint16_t* out;
+  int64_t ld_out, out_rows;
 };
 
 hipError_t launch_compact(const uint8_t* mask, int64_t n_rows, int32_t* rows,
                           int32_t* n_scored, float* logp, float* lse, float* entropy,
                           hipStream_t stream);
 hipError_t launch_lmhead(const LmheadArgs& a, int64_t grid, bool bf16, hipStream_t stream);
+hipError_t launch_lmhead_grad(const LmheadArgs& a, int64_t grid, hipStream_t stream);
+hipError_t launch_gemm_nt(const GemmArgs& a, hipStream_t stream);
+hipError_t launch_transpose(const TransposeArgs& a, hipStream_t stream);
+// dh[map[e]][j] = sum_s part[s][e][j] for e < clamp(*dyn - dyn_base, 0, cap)
+hipError_t launch_splitk_scatter(const float* part, int64_t splits, int64_t split_stride, int64_t d,
+                                 const int32_t* map, const int32_t* dyn, int64_t dyn_base, int64_t cap,
+                                 float* dh, hipStream_t stream);
+// dh[n][:] = 0 for rows with mask[n] == 0
+hipError_t launch_zero_masked_rows(const uint8_t* mask, int64_t n_rows, int64_t d, float* dh,
+                                   hipStream_t stream);
 hipError_t launch_merge(const LmheadArgs& a, int64_t n_rows, float* logp, float* lse,
                         float* entropy, hipStream_t stream);
 // values == true: rank `lo` itself (lh unused); otherwise rank |lh - lo|.

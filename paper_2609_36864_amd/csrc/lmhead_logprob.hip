@@ -37,130 +37,15 @@
 // 16-byte K fragment chosen by (l div 32); A and B fragments use the same K
 // assignment, so the contraction is exact whatever order the hardware sums
 // the K values in.
-#include "hdl_internal.h"
+#include "tile_common.h"
 
 #include <type_traits>
 
 namespace hdl {
 namespace {
 
-typedef __bf16 bf16x8_t __attribute__((ext_vector_type(8)));
-typedef float f32x16_t __attribute__((ext_vector_type(16)));
+using namespace tile;
 
-#ifndef HDL_WAVES
-#define HDL_WAVES 8
-#endif
-constexpr int kWaves = HDL_WAVES;                   // 4: one wave per SIMD; 8: two
-constexpr int kThreads = 64 * kWaves;
-constexpr int kNB = kWaves == 4 ? 4 : 2;            // 32-token MFMA blocks per wave
-constexpr int kWaveN = 32 * kNB;                    // tokens per wave (128 or 64)
-#ifndef HDL_LDS_CHUNKS
-#define HDL_LDS_CHUNKS 8
-#endif
-#ifndef HDL_LDS_STAGES
-#define HDL_LDS_STAGES 2
-#endif
-constexpr int kChunks = HDL_LDS_CHUNKS;             // 16-byte chunks per LDS row per stage
-constexpr int kStages = HDL_LDS_STAGES;             // LDS ring depth (K-slices)
-constexpr int kSlots = kTileV * kChunks;            // uint4 slots per operand per stage
-constexpr int kBlockRows = 64 / kChunks;            // rows per 1 KB DMA block
-constexpr int kBlocksPerWave = kTileV / kBlockRows / kWaves;   // DMA blocks per operand per wave
-constexpr int kDmaPerSlice = 2 * kBlocksPerWave;    // DMA instructions per lane per slice
-constexpr int kSub = kChunks / 2;                   // MFMA sub-steps per slice
-constexpr float kLog2e = 1.4426950408889634f;
-constexpr float kNegInf = -__builtin_inff();
-
-static_assert(kTileV == kTileN, "square workgroup tile assumed");
-static_assert(kWaves == 4 || kWaves == 8, "4 or 8 waves");
-static_assert(kChunks == 4 || kChunks == 8, "64- or 128-byte K-slices");
-static_assert(kStages * 2 * kSlots * 16 <= 160 * 1024, "LDS ring exceeds 160 KB");
-static_assert(kDmaPerSlice * (kStages - 1) <= 63, "vmcnt range");
-
-#ifndef HDL_SWZ
-#define HDL_SWZ 1
-#endif
-// XOR pattern of a row: the rows of one 32-row fragment read must land in
-// distinct 16-byte bank groups whether the LDS serves 8 or 16 lanes of a
-// ds_read_b128 per cycle.  With 128-byte rows, (row & 7) ^ ((row >> 3) & 1)
-// does both: 8 consecutive rows get 8 distinct chunks, and rows r and r+8
-// (same bank half when two rows share a 256-byte bank line) differ too.
-__device__ __forceinline__ int row_xor(int row) {
-  if (kChunks == 8) {
-    if (HDL_SWZ == 0) return row & 7;
-    if (HDL_SWZ == 1) return (row & 7) ^ ((row >> 3) & 1);
-    return (row >> 1) & 7;
-  }
-  if (HDL_SWZ == 0) return (row >> 1) & 3;
-  if (HDL_SWZ == 1) return ((row >> 1) & 3) ^ ((row >> 3) & 1);
-  return (row >> 2) & 3;
-}
-
-// Slot of (row, logical 16-byte chunk) in a [rows][kChunks] LDS tile.
-__device__ __forceinline__ int swz(int row, int chunk) {
-  return row * kChunks + (chunk ^ row_xor(row));
-}
-
-__device__ __forceinline__ float fast_exp2(float x) { return __builtin_amdgcn_exp2f(x); }
-
-// 16 bytes per lane from global memory straight into LDS at lds_base + 16*lane.
-// The global address is a wave-uniform 64-bit base (SGPRs) plus a per-lane
-// 32-bit byte offset, so issuing a DMA costs no vector ALU work.  M0 carries
-// the LDS base; it is saved and restored around the DMA so the compiler's own
-// use of M0 is unaffected.
-__device__ __forceinline__ void dma16(uint64_t sbase, uint32_t voff, uint32_t lds_base) {
-  uint32_t saved;
-  asm volatile(
-      "s_mov_b32 %0, m0\n\t"
-      "s_mov_b32 m0, %1\n\t"
-      "s_nop 0\n\t"
-      "global_load_lds_dwordx4 %2, %3\n\t"
-      "s_mov_b32 m0, %0"
-      : "=&s"(saved)
-      : "s"(lds_base), "v"(voff), "s"(sbase)
-      : "memory");
-}
-
-// Wait until at most `slices` K-slices of this lane's DMA are outstanding.
-template <int N>
-__device__ __forceinline__ void wait_vmcnt() {
-  asm volatile("s_waitcnt vmcnt(%0)" ::"n"(N) : "memory");
-}
-__device__ __forceinline__ void wait_dma(int slices) {
-  if (kStages > 3 && slices >= 3) wait_vmcnt<(kStages > 3 ? 3 : 0) * kDmaPerSlice>();
-  else if (kStages > 2 && slices >= 2) wait_vmcnt<(kStages > 2 ? 2 : 0) * kDmaPerSlice>();
-  else if (slices >= 1) wait_vmcnt<kDmaPerSlice>();
-  else wait_vmcnt<0>();
-}
-
-// Workgroup barrier without the memory fence __syncthreads() implies (the
-// fence would wait for every in-flight DMA).  LDS reads issued before it
-// are complete: callers wait lgkmcnt(0) first.
-__device__ __forceinline__ void raw_barrier() {
-  asm volatile("s_waitcnt lgkmcnt(0)\n\ts_barrier" ::: "memory");
-}
-
-// One MFMA step over a pair of 16-byte fragments (same K positions in A, B).
-template <bool BF16> struct Mma;
-
-template <> struct Mma<true> {
-  static constexpr int kElemsPer16B = 8;
-  __device__ __forceinline__ static void run(const uint4& a, const uint4& b, f32x16_t& c) {
-    c = __builtin_amdgcn_mfma_f32_32x32x16_bf16(__builtin_bit_cast(bf16x8_t, a),
-                                                __builtin_bit_cast(bf16x8_t, b), c, 0, 0, 0);
-  }
-};
-
-template <> struct Mma<false> {
-  static constexpr int kElemsPer16B = 4;
-  // Four K=2 steps; lane group g supplies K offset 4g + j in step j, the same
-  // for both operands, so the four steps cover the fragment's 8 K values.
-  __device__ __forceinline__ static void run(const uint4& a, const uint4& b, f32x16_t& c) {
-    c = __builtin_amdgcn_mfma_f32_32x32x2f32(__uint_as_float(a.x), __uint_as_float(b.x), c, 0, 0, 0);
-    c = __builtin_amdgcn_mfma_f32_32x32x2f32(__uint_as_float(a.y), __uint_as_float(b.y), c, 0, 0, 0);
-    c = __builtin_amdgcn_mfma_f32_32x32x2f32(__uint_as_float(a.z), __uint_as_float(b.z), c, 0, 0, 0);
-    c = __builtin_amdgcn_mfma_f32_32x32x2f32(__uint_as_float(a.w), __uint_as_float(b.w), c, 0, 0, 0);
-  }
-};
 
 // t of a state, moved from its own max m to a larger max mn:
 //   sum exp(z - mn) * (z - mn) log2(e) = f * (t + (m - mn) log2(e) * s),  f = exp(m - mn).
@@ -189,16 +74,23 @@ __device__ __forceinline__ void combine(float& m, float& s, float& z, float& t, 
   z = fmaxf(z, z2);
 }
 
-// Row of the 32x32 accumulator block held in element i of lane l:
-// row = 8*(i/4) + 4*(l/32) + (i%4), column = l%32.
-__device__ __forceinline__ int acc_row(int i, int half) { return 8 * (i >> 2) + 4 * half + (i & 3); }
 
 // KTAIL: d is not a multiple of the K-slice, so the last slice of every
 // row needs zero-filling (a separate instantiation keeps that work out of the
-// common case).  ENT: also accumulate sum exp(z - m) * (z - m) for the next-token
-// entropy H = ln s - E_p[z - m] (the Entropy localization baseline).
-template <bool BF16, bool KTAIL, bool ENT>
+// common case).  EPI selects what each V-tile's logits feed:
+//   kEpiStats:   online max / sum of exp and the sampled-token logit;
+//   kEpiEntropy: the same plus sum exp(z - m) * (z - m) for the next-token
+//                entropy H = ln s - E_p[z - m] (the Entropy localization
+//                baseline);
+//   kEpiGrad:    the gradient of log p with respect to the logits,
+//                g (1[v == y] - exp(z - lse)), written as bf16 (backward pass;
+//                lse comes from the forward pass).
+constexpr int kEpiStats = 0, kEpiEntropy = 1, kEpiGrad = 2;
+
+template <bool BF16, bool KTAIL, int EPI>
 __global__ __launch_bounds__(kThreads, 1) void lmhead_logprob_kernel(LmheadArgs p) {
+  constexpr bool ENT = EPI == kEpiEntropy;
+  constexpr bool GRAD = EPI == kEpiGrad;
   using M = Mma<BF16>;
   constexpr int kEsz = BF16 ? 2 : 4;
   constexpr int kSliceK = M::kElemsPer16B * kChunks;   // K elements per slice
@@ -216,7 +108,7 @@ __global__ __launch_bounds__(kThreads, 1) void lmhead_logprob_kernel(LmheadArgs 
   // ---- work item: XCD-aware (row tile, vocabulary chunk) ------------------
   // Workgroups are dealt to the XCDs round-robin.  The j-th workgroup of an
   // XCD belongs to launch group (j / 32) of that XCD; a group is a block of
-  // 4 row tiles x 8 vocabulary chunks, so the workgroups resident on one XCD
+  // kGroupRT row tiles x kGroupCH vocabulary chunks, so the workgroups resident on one XCD
   // at a time share hidden tiles and W tiles through that XCD's L2.
   const int64_t b = blockIdx.x;
   const int64_t xcd = b % kNumXcd;
@@ -225,7 +117,8 @@ __global__ __launch_bounds__(kThreads, 1) void lmhead_logprob_kernel(LmheadArgs 
   const int loc = static_cast<int>(j % (kGroupRT * kGroupCH));
   const int64_t rt = (grp % p.n_grt) * kGroupRT + (loc % kGroupRT);
   const int64_t ch = (grp / p.n_grt) * kGroupCH + (loc / kGroupRT);
-  const int64_t n_s = *p.n_scored;
+  int64_t n_s = *p.n_scored - p.row_base;
+  n_s = n_s < 0 ? 0 : (n_s > p.row_cap ? p.row_cap : n_s);
   const int64_t n_rt = (n_s + kTileN - 1) / kTileN;
   if (rt >= n_rt || ch >= p.n_ch) return;
 
@@ -241,11 +134,17 @@ __global__ __launch_bounds__(kThreads, 1) void lmhead_logprob_kernel(LmheadArgs 
 
   // ---- this lane's token columns and their sampled tokens ------------------
   int tok[kNB];
+  float g_lse[kNB], g_up[kNB];   // gradient mode: lse * log2(e) and upstream gradient
 #pragma unroll
   for (int bn = 0; bn < kNB; ++bn) {
     int64_t e = rt * kTileN + wn * kWaveN + bn * 32 + col;
     e = e < n_s ? e : n_s - 1;
-    tok[bn] = p.tokens[p.rows[e]];
+    const int row = p.rows[e];
+    tok[bn] = p.tokens[row];
+    if (GRAD) {
+      g_lse[bn] = p.lse_in[row] * kLog2e;
+      g_up[bn] = p.grad_in[row];
+    }
   }
 
   float run_m[kNB], run_s[kNB], run_z[kNB], run_t[kNB];
@@ -430,6 +329,45 @@ __global__ __launch_bounds__(kThreads, 1) void lmhead_logprob_kernel(LmheadArgs 
         for (int q = 0; q < 16; ++q) acc[bm][bn][q] = 0.f;
   };
 
+  // Gradient mode: G = g (1[v == y] - p) for the 4 x kNB blocks of this wave,
+  // rounded to bf16 and stored as 4 consecutive vocabulary entries (8 bytes)
+  // per accumulator run.  Rows >= V hold -inf, so p = 0 and G = 0 there,
+  // which zero-fills the columns up to g_cols.
+  auto grad_epilogue = [&](int64_t vt) {
+    const int64_t vbase = vt * kTileV + wm * 128;
+#pragma unroll
+    for (int bn = 0; bn < kNB; ++bn) {
+      const int64_t e = rt * kTileN + wn * kWaveN + bn * 32 + col;
+      uint16_t* grow = p.g_out + e * p.g_ld;
+#pragma unroll
+      for (int bm = 0; bm < 4; ++bm)
+#pragma unroll
+        for (int jr = 0; jr < 4; ++jr) {
+          const int64_t v0 = vbase + bm * 32 + 8 * jr + 4 * half;
+          uint32_t packed[2];
+#pragma unroll
+          for (int r = 0; r < 4; r += 2) {
+            float gv[2];
+#pragma unroll
+            for (int u = 0; u < 2; ++u) {
+              const float pv = fast_exp2(__builtin_fmaf(acc[bm][bn][jr * 4 + r + u], kLog2e, -g_lse[bn]));
+              gv[u] = (v0 + r + u == tok[bn]) ? g_up[bn] * (1.f - pv) : -g_up[bn] * pv;
+            }
+            packed[r / 2] = static_cast<uint32_t>(__builtin_bit_cast(uint16_t, static_cast<__bf16>(gv[0]))) |
+                            (static_cast<uint32_t>(__builtin_bit_cast(uint16_t, static_cast<__bf16>(gv[1]))) << 16);
+          }
+          if (e < n_s && v0 < p.g_cols)
+            *reinterpret_cast<uint2*>(grow + v0) = make_uint2(packed[0], packed[1]);
+        }
+    }
+#pragma unroll
+    for (int bm = 0; bm < 4; ++bm)
+#pragma unroll
+      for (int bn = 0; bn < kNB; ++bn)
+#pragma unroll
+        for (int q = 0; q < 16; ++q) acc[bm][bn][q] = 0.f;
+  };
+
   // ---- pipelined main loop over (V-tile, K-slice) ------------------------
   const int n_pre = n_iter < kStages ? n_iter : kStages;
   for (int sl = 0; sl < n_pre; ++sl) issue(sl);
@@ -494,11 +432,27 @@ __global__ __launch_bounds__(kThreads, 1) void lmhead_logprob_kernel(LmheadArgs 
         }
       }
     }
-    if ((vt + 1) * kTileV <= V) epilogue(vt, std::false_type{});
-    else epilogue(vt, std::true_type{});
+    if (GRAD) {
+      if ((vt + 1) * kTileV > V) {
+        // rows >= V: -inf, so that they contribute G = 0
+#pragma unroll
+        for (int bm = 0; bm < 4; ++bm)
+#pragma unroll
+          for (int bn = 0; bn < kNB; ++bn)
+#pragma unroll
+            for (int q = 0; q < 16; ++q)
+              if (vt * kTileV + wm * 128 + bm * 32 + acc_row(q, half) >= V) acc[bm][bn][q] = kNegInf;
+      }
+      grad_epilogue(vt);
+    } else if ((vt + 1) * kTileV <= V) {
+      epilogue(vt, std::false_type{});
+    } else {
+      epilogue(vt, std::true_type{});
+    }
   }
   wait_vmcnt<0>();   // (dummy DMAs past the end may still be landing)
   __syncthreads();
+  if (GRAD) return;
 
   // ---- merge the two lane halves, then the two vocabulary waves -----------
 #pragma unroll
@@ -584,15 +538,25 @@ hipError_t launch_lmhead(const LmheadArgs& a, int64_t grid, bool bf16, hipStream
   const bool ent = a.part_t != nullptr;
   const int which = (bf16 ? 4 : 0) + (tail ? 2 : 0) + (ent ? 1 : 0);
   switch (which) {
-    case 0: hipLaunchKernelGGL((lmhead_logprob_kernel<false, false, false>), g, b, 0, stream, a); break;
-    case 1: hipLaunchKernelGGL((lmhead_logprob_kernel<false, false, true>), g, b, 0, stream, a); break;
-    case 2: hipLaunchKernelGGL((lmhead_logprob_kernel<false, true, false>), g, b, 0, stream, a); break;
-    case 3: hipLaunchKernelGGL((lmhead_logprob_kernel<false, true, true>), g, b, 0, stream, a); break;
-    case 4: hipLaunchKernelGGL((lmhead_logprob_kernel<true, false, false>), g, b, 0, stream, a); break;
-    case 5: hipLaunchKernelGGL((lmhead_logprob_kernel<true, false, true>), g, b, 0, stream, a); break;
-    case 6: hipLaunchKernelGGL((lmhead_logprob_kernel<true, true, false>), g, b, 0, stream, a); break;
-    default: hipLaunchKernelGGL((lmhead_logprob_kernel<true, true, true>), g, b, 0, stream, a); break;
+    case 0: hipLaunchKernelGGL((lmhead_logprob_kernel<false, false, kEpiStats>), g, b, 0, stream, a); break;
+    case 1: hipLaunchKernelGGL((lmhead_logprob_kernel<false, false, kEpiEntropy>), g, b, 0, stream, a); break;
+    case 2: hipLaunchKernelGGL((lmhead_logprob_kernel<false, true, kEpiStats>), g, b, 0, stream, a); break;
+    case 3: hipLaunchKernelGGL((lmhead_logprob_kernel<false, true, kEpiEntropy>), g, b, 0, stream, a); break;
+    case 4: hipLaunchKernelGGL((lmhead_logprob_kernel<true, false, kEpiStats>), g, b, 0, stream, a); break;
+    case 5: hipLaunchKernelGGL((lmhead_logprob_kernel<true, false, kEpiEntropy>), g, b, 0, stream, a); break;
+    case 6: hipLaunchKernelGGL((lmhead_logprob_kernel<true, true, kEpiStats>), g, b, 0, stream, a); break;
+    default: hipLaunchKernelGGL((lmhead_logprob_kernel<true, true, kEpiEntropy>), g, b, 0, stream, a); break;
   }
+  return hipGetLastError();
+}
+
+hipError_t launch_lmhead_grad(const LmheadArgs& a, int64_t grid, hipStream_t stream) {
+  if (grid <= 0) return hipSuccess;
+  const dim3 g(static_cast<unsigned>(grid)), b(kThreads);
+  if (a.d % (8 * kChunks) != 0)
+    hipLaunchKernelGGL((lmhead_logprob_kernel<true, true, kEpiGrad>), g, b, 0, stream, a);
+  else
+    hipLaunchKernelGGL((lmhead_logprob_kernel<true, false, kEpiGrad>), g, b, 0, stream, a);
   return hipGetLastError();
 }
 

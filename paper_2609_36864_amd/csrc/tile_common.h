@@ -1,0 +1,136 @@
+// Building blocks shared by the MFMA tile kernels of libhdl.so (the fused
+// lm-head kernel and the plain NT GEMM of the backward pass): the 256 x 256
+// workgroup tile, its LDS ring of K-slices with XOR-swizzled 16-byte chunks,
+// the direct global -> LDS DMA, explicit memory-counter waits, and the MFMA
+// step for bf16 and fp32 operands.  Not part of the public ABI.
+#pragma once
+
+#include "hdl_internal.h"
+
+namespace hdl {
+namespace tile {
+
+typedef __bf16 bf16x8_t __attribute__((ext_vector_type(8)));
+typedef float f32x16_t __attribute__((ext_vector_type(16)));
+
+#ifndef HDL_WAVES
+#define HDL_WAVES 8
+#endif
+constexpr int kWaves = HDL_WAVES;                   // 4: one wave per SIMD; 8: two
+constexpr int kThreads = 64 * kWaves;
+constexpr int kNB = kWaves == 4 ? 4 : 2;            // 32-token MFMA blocks per wave
+constexpr int kWaveN = 32 * kNB;                    // tokens per wave (128 or 64)
+#ifndef HDL_LDS_CHUNKS
+#define HDL_LDS_CHUNKS 8
+#endif
+#ifndef HDL_LDS_STAGES
+#define HDL_LDS_STAGES 2
+#endif
+constexpr int kChunks = HDL_LDS_CHUNKS;             // 16-byte chunks per LDS row per stage
+constexpr int kStages = HDL_LDS_STAGES;             // LDS ring depth (K-slices)
+constexpr int kSlots = kTileV * kChunks;            // uint4 slots per operand per stage
+constexpr int kBlockRows = 64 / kChunks;            // rows per 1 KB DMA block
+constexpr int kBlocksPerWave = kTileV / kBlockRows / kWaves;   // DMA blocks per operand per wave
+constexpr int kDmaPerSlice = 2 * kBlocksPerWave;    // DMA instructions per lane per slice
+constexpr int kSub = kChunks / 2;                   // MFMA sub-steps per slice
+constexpr float kLog2e = 1.4426950408889634f;
+constexpr float kNegInf = -__builtin_inff();
+
+static_assert(kTileV == kTileN, "square workgroup tile assumed");
+static_assert(kWaves == 4 || kWaves == 8, "4 or 8 waves");
+static_assert(kChunks == 4 || kChunks == 8, "64- or 128-byte K-slices");
+static_assert(kStages * 2 * kSlots * 16 <= 160 * 1024, "LDS ring exceeds 160 KB");
+static_assert(kDmaPerSlice * (kStages - 1) <= 63, "vmcnt range");
+
+#ifndef HDL_SWZ
+#define HDL_SWZ 1
+#endif
+// XOR pattern of a row: the rows of one 32-row fragment read must land in
+// distinct 16-byte bank groups whether the LDS serves 8 or 16 lanes of a
+// ds_read_b128 per cycle.  With 128-byte rows, (row & 7) ^ ((row >> 3) & 1)
+// does both: 8 consecutive rows get 8 distinct chunks, and rows r and r+8
+// (same bank half when two rows share a 256-byte bank line) differ too.
+__device__ __forceinline__ int row_xor(int row) {
+  if (kChunks == 8) {
+    if (HDL_SWZ == 0) return row & 7;
+    if (HDL_SWZ == 1) return (row & 7) ^ ((row >> 3) & 1);
+    return (row >> 1) & 7;
+  }
+  if (HDL_SWZ == 0) return (row >> 1) & 3;
+  if (HDL_SWZ == 1) return ((row >> 1) & 3) ^ ((row >> 3) & 1);
+  return (row >> 2) & 3;
+}
+
+// Slot of (row, logical 16-byte chunk) in a [rows][kChunks] LDS tile.
+__device__ __forceinline__ int swz(int row, int chunk) {
+  return row * kChunks + (chunk ^ row_xor(row));
+}
+
+__device__ __forceinline__ float fast_exp2(float x) { return __builtin_amdgcn_exp2f(x); }
+
+// 16 bytes per lane from global memory straight into LDS at lds_base + 16*lane.
+// The global address is a wave-uniform 64-bit base (SGPRs) plus a per-lane
+// 32-bit byte offset, so issuing a DMA costs no vector ALU work.  M0 carries
+// the LDS base; it is saved and restored around the DMA so the compiler's own
+// use of M0 is unaffected.
+__device__ __forceinline__ void dma16(uint64_t sbase, uint32_t voff, uint32_t lds_base) {
+  uint32_t saved;
+  asm volatile(
+      "s_mov_b32 %0, m0\n\t"
+      "s_mov_b32 m0, %1\n\t"
+      "s_nop 0\n\t"
+      "global_load_lds_dwordx4 %2, %3\n\t"
+      "s_mov_b32 m0, %0"
+      : "=&s"(saved)
+      : "s"(lds_base), "v"(voff), "s"(sbase)
+      : "memory");
+}
+
+// Wait until at most `slices` K-slices of this lane's DMA are outstanding.
+template <int N>
+__device__ __forceinline__ void wait_vmcnt() {
+  asm volatile("s_waitcnt vmcnt(%0)" ::"n"(N) : "memory");
+}
+__device__ __forceinline__ void wait_dma(int slices) {
+  if (kStages > 3 && slices >= 3) wait_vmcnt<(kStages > 3 ? 3 : 0) * kDmaPerSlice>();
+  else if (kStages > 2 && slices >= 2) wait_vmcnt<(kStages > 2 ? 2 : 0) * kDmaPerSlice>();
+  else if (slices >= 1) wait_vmcnt<kDmaPerSlice>();
+  else wait_vmcnt<0>();
+}
+
+// Workgroup barrier without the memory fence __syncthreads() implies (the
+// fence would wait for every in-flight DMA).  LDS reads issued before it
+// are complete: callers wait lgkmcnt(0) first.
+__device__ __forceinline__ void raw_barrier() {
+  asm volatile("s_waitcnt lgkmcnt(0)\n\ts_barrier" ::: "memory");
+}
+
+// One MFMA step over a pair of 16-byte fragments (same K positions in A, B).
+template <bool BF16> struct Mma;
+
+template <> struct Mma<true> {
+  static constexpr int kElemsPer16B = 8;
+  __device__ __forceinline__ static void run(const uint4& a, const uint4& b, f32x16_t& c) {
+    c = __builtin_amdgcn_mfma_f32_32x32x16_bf16(__builtin_bit_cast(bf16x8_t, a),
+                                                __builtin_bit_cast(bf16x8_t, b), c, 0, 0, 0);
+  }
+};
+
+template <> struct Mma<false> {
+  static constexpr int kElemsPer16B = 4;
+  // Four K=2 steps; lane group g supplies K offset 4g + j in step j, the same
+  // for both operands, so the four steps cover the fragment's 8 K values.
+  __device__ __forceinline__ static void run(const uint4& a, const uint4& b, f32x16_t& c) {
+    c = __builtin_amdgcn_mfma_f32_32x32x2f32(__uint_as_float(a.x), __uint_as_float(b.x), c, 0, 0, 0);
+    c = __builtin_amdgcn_mfma_f32_32x32x2f32(__uint_as_float(a.y), __uint_as_float(b.y), c, 0, 0, 0);
+    c = __builtin_amdgcn_mfma_f32_32x32x2f32(__uint_as_float(a.z), __uint_as_float(b.z), c, 0, 0, 0);
+    c = __builtin_amdgcn_mfma_f32_32x32x2f32(__uint_as_float(a.w), __uint_as_float(b.w), c, 0, 0, 0);
+  }
+};
+
+// Row of the 32x32 accumulator block held in element i of lane l:
+// row = 8*(i/4) + 4*(l/32) + (i%4), column = l%32.
+__device__ __forceinline__ int acc_row(int i, int half) { return 8 * (i >> 2) + 4 * half + (i & 3); }
+
+}  // namespace tile
+}  // namespace hdl

@@ -30,7 +30,7 @@ def test_header_declares_the_boundary():
     names = _declared_functions()
     for n in ("hdl_token_logprobs", "hdl_token_logprobs_entropy", "hdl_select_branch_points",
               "hdl_select_top_k", "hdl_token_logprobs_workspace_size", "hdl_status_string",
-              "hdl_last_error"):
+              "hdl_last_error", "hdl_token_logprobs_backward", "hdl_token_logprobs_backward_workspace_size"):
         assert n in names
 
 
@@ -43,7 +43,7 @@ def test_status_strings(lib):
     assert lib.hdl_status_string(0) == b"ok"
     for s in (-1, -2, -3, -4):
         assert lib.hdl_status_string(s) not in (b"ok", b"unknown status")
-    assert lib.hdl_abi_version() == 2
+    assert lib.hdl_abi_version() == 3
 
 
 def test_workspace_size_rules(lib):
@@ -90,3 +90,26 @@ def test_entropy_and_value_topk_argument_errors(lib):
     assert g(None, None, 1, 10, 2, p, p, p, None) == -1
     assert g(p, None, 1, 10, 0, p, p, p, None) == -1
     assert g(p, None, 1, 10, 1025, p, p, p, None) == -2
+
+
+def test_backward_workspace_and_argument_errors(lib):
+    ws = lib.hdl_token_logprobs_backward_workspace_size
+    ws.restype = ctypes.c_size_t
+    ws.argtypes = [ctypes.c_int64, ctypes.c_int64, ctypes.c_int64, ctypes.c_int]
+    # one chunk of G and its transpose dominate: 4 * rows * round_up(V, 64) bytes
+    n, d, V = 1000, 64, 1000
+    size = ws(n, d, V, 1)
+    assert size >= 4 * 1024 * 1024 and size < 4 * 1024 * 1024 + 8 * 1024 * 1024
+    assert ws(n, d, V, 0) == 0          # fp32 inputs are not supported
+    assert ws(n, 12, V, 1) == 0         # d not a multiple of 8
+    assert ws(0, d, V, 1) == 0
+    f = lib.hdl_token_logprobs_backward
+    f.restype = ctypes.c_int
+    f.argtypes = [ctypes.c_void_p] * 6 + [ctypes.c_int64] * 3 + [ctypes.c_int, ctypes.c_void_p, ctypes.c_void_p,
+                                                                 ctypes.c_int, ctypes.c_void_p, ctypes.c_size_t,
+                                                                 ctypes.c_void_p]
+    p = ctypes.c_void_p(4096)
+    assert f(p, p, p, None, p, None, n, d, V, 1, p, p, 0, p, size, None) == -1   # null grad_logp
+    assert f(p, p, p, None, p, p, n, d, V, 0, p, p, 0, p, size, None) == -2      # fp32
+    assert f(p, p, p, None, p, p, n, d, V, 1, p, p, 0, p, size - 256, None) == -3
+    assert f(p, p, p, None, p, p, n, d, V, 1, p, p, 0, ctypes.c_void_p(4096 + 16), size, None) == -1

@@ -423,3 +423,75 @@ def test_entropy_is_lse_minus_expected_logit():
     m = np.array([1, 0, 1, 0, 1], np.uint8)
     H = O.token_entropy(h, W, m)
     assert np.all(H[m == 0] == 0.0) and np.all(H <= np.log(700) + 1e-12)
+
+
+# ------------------------------------------------------------ backward pass
+def _loss(H, W, y, g):
+    # L = sum_n g_n log p_n(y_n), written with the library-free log-sum-exp
+    z = H @ W.T
+    out = 0.0
+    for n in range(H.shape[0]):
+        zn = z[n]
+        m = max(zn)
+        lse = m + math.log(math.fsum(math.exp(v - m) for v in zn))
+        out += g[n] * (zn[y[n]] - lse)
+    return out
+
+
+def test_backward_matches_central_differences():
+    # the gradient of L by central differences in every coordinate of H and W
+    rng = np.random.default_rng(21)
+    N, V, d = 4, 7, 3
+    H = rng.normal(size=(N, d))
+    W = rng.normal(size=(V, d))
+    y = rng.integers(0, V, N)
+    g = rng.normal(size=N)
+    dH, dW, _, _ = O.token_logprobs_backward(H, W, y, g)
+    h = 1e-6
+    for arr, grad in ((H, dH), (W, dW)):
+        num = np.zeros_like(arr)
+        for idx in np.ndindex(arr.shape):
+            old = arr[idx]
+            arr[idx] = old + h
+            lp = _loss(H, W, y, g)
+            arr[idx] = old - h
+            lm = _loss(H, W, y, g)
+            arr[idx] = old
+            num[idx] = (lp - lm) / (2 * h)
+        assert np.allclose(grad, num, rtol=1e-6, atol=1e-7)
+
+
+def test_backward_closed_forms_and_invariants():
+    rng = np.random.default_rng(22)
+    N, V, d = 6, 9, 4
+    H = rng.normal(size=(N, d))
+    W = rng.normal(size=(V, d))
+    y = rng.integers(0, V, N)
+    g = rng.normal(size=N)
+    dH, dW, mH, mW = O.token_logprobs_backward(H, W, y, g)
+    # probabilities sum to one, so the vocabulary rows of dW sum to zero
+    assert np.allclose(dW.sum(axis=0), 0.0, atol=1e-12)
+    # identical W rows: uniform softmax, dH_n = g_n (W_y - mean W) = 0
+    Wc = np.tile(rng.normal(size=(1, d)), (V, 1))
+    dHc, _, _, _ = O.token_logprobs_backward(H, Wc, y, g)
+    assert np.allclose(dHc, 0.0, atol=1e-12)
+    # two words: d log sigmoid(z0 - z1) / d z0 = 1 - sigmoid(z0 - z1)
+    W2 = np.array([[1.0, 0.0], [0.0, 1.0]])
+    h2 = np.array([[0.7, -0.2]])
+    sig = 1 / (1 + math.exp(-(0.7 + 0.2)))
+    dH2, _, _, _ = O.token_logprobs_backward(h2, W2, np.array([0]), np.array([1.0]))
+    assert np.allclose(dH2[0], [1 - sig, -(1 - sig)], atol=1e-15)
+    # masked rows: zero dH, no contribution to dW; magnitudes dominate results
+    mask = np.array([1, 0, 1, 1, 0, 1], np.uint8)
+    dHm, dWm, _, _ = O.token_logprobs_backward(H, W, y, g, mask)
+    assert np.all(dHm[mask == 0] == 0)
+    keep = mask != 0
+    _, dWk, _, _ = O.token_logprobs_backward(H[keep], W, y[keep], g[keep])
+    assert np.allclose(dWm, dWk, atol=1e-13)
+    assert np.all(np.abs(dH) <= mH + 1e-15) and np.all(np.abs(dW) <= mW + 1e-15)
+    # an out-of-range token has no indicator term
+    y_bad = y.copy(); y_bad[0] = V
+    dHb, _, _, _ = O.token_logprobs_backward(H[:1], W, y_bad[:1], g[:1])
+    z = H[0] @ W.T
+    p = np.exp(z - z.max()); p /= p.sum()
+    assert np.allclose(dHb[0], -g[0] * (p @ W), atol=1e-13)
