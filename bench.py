@@ -33,6 +33,7 @@ METRIC = "scored tokens/sec (both contexts) + MFMA util of fused lm-head logprob
 METRIC_ENTROPY = "scored tokens/sec (original context) of fused lm-head entropy + top-k (Entropy baseline)"
 # Training side: gradients of the token-level policy loss (Sec. 3.3) through the lm-head.
 METRIC_BACKWARD = "trained tokens/sec of the lm-head backward (dL/dh, dL/dW) + MFMA util"
+METRIC_GROUP = "trained tokens/sec of group construction (constrained selection, 3+4 allocation, advantages, policy-loss factors)"
 
 
 def log(msg: str) -> None:
@@ -131,6 +132,9 @@ def main() -> int:
     ap.add_argument("--backward", action="store_true",
                     help="time the backward pass (gradients with respect to the hidden states and the "
                          "lm-head weight) on the original-context rows instead of the re-scoring step")
+    ap.add_argument("--group", action="store_true",
+                    help="time localized group construction: constrained branch-point selection, "
+                         "continuation allocation, group advantages and per-token policy-loss factors")
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--cpu-budget", type=float, default=15.0)
     ap.add_argument("--no-mfma-ceiling", action="store_true",
@@ -164,6 +168,8 @@ def main() -> int:
 
     if args.backward:
         return bench_backward(args, w, hdl, dev)
+    if args.group:
+        return bench_group(args, w, hdl, dev)
 
     ent_sel = args.selector == "entropy"
     n_keep = c.R * c.T if ent_sel else 2 * c.R * c.T   # rows are [context][root][t]
@@ -377,6 +383,119 @@ def bench_backward(args, w, hdl, dev) -> int:
     if not args.no_cpu_baseline:
         log("timing the float64 oracle backward on a bounded sample")
         result["cpu_baseline"] = cpu_baseline_backward(w, budget_s=args.cpu_budget)
+    print(json.dumps(result), flush=True)
+    return 0
+
+
+def bench_group(args, w, hdl, dev) -> int:
+    """One training step's group construction at the paper's batch (128
+    problems, 2 roots + 14 continuations each, Sec. 4.1) with the workload's
+    trajectory length T: the 256 roots' log p pairs (synthetic, as the
+    re-scoring step would leave them) are ranked under the branch-point
+    constraints (spacing 64, index range excluding the first and last 32
+    positions), 3 + 4 continuations are allocated per root, every group gets
+    mean-centred advantages, and every token of every trajectory (T each; a
+    continuation trains only its suffix) gets its clipped-loss factor."""
+    import numpy as np
+    import torch
+    import workloads
+    c = w.cfg
+    n_groups, roots_per_group, alloc = 128, 2, (3, 4)
+    R, T = n_groups * roots_per_group, c.T
+    lo_, hi_, mask = workloads.make_logp_pair(R, T, seed=c.seed + 11)
+    lo_t = torch.from_numpy(lo_).to(dev)
+    hi_t = torch.from_numpy(hi_).to(dev)
+    mask_t = torch.from_numpy(mask).to(dev)
+    rlo = torch.full((R,), 32, dtype=torch.int32, device=dev)
+    rhi = torch.full((R,), T - 33, dtype=torch.int32, device=dev)
+    G = roots_per_group * (1 + sum(alloc))
+    n_traj = n_groups * G
+    rng = np.random.default_rng(c.seed + 12)
+    rewards = torch.from_numpy((rng.random((n_groups, G)) < 0.5).astype(np.float32)).to(dev)
+    n_tok = n_traj * T
+    traj = torch.arange(n_traj, dtype=torch.int32, device=dev).repeat_interleave(T)
+    pos = torch.arange(T, dtype=torch.int32, device=dev).repeat(n_traj)
+    logp_old = torch.from_numpy((-rng.exponential(2.0, n_tok)).astype(np.float32)).to(dev)
+    logp_new = logp_old + torch.from_numpy((rng.normal(size=n_tok) * 0.2).astype(np.float32)).to(dev)
+    tmask = torch.from_numpy((rng.random(n_tok) < 0.9).astype(np.uint8)).to(dev)
+    start = torch.zeros(n_traj, dtype=torch.int32, device=dev)
+    grad = torch.empty(n_tok, dtype=torch.float32, device=dev)
+    torch.cuda.synchronize()
+
+    def step():
+        idx, score, count = hdl.select_constrained(lo_t, hi_t, mask_t, len(alloc), lo=rlo, hi=rhi, min_gap=64)
+        bpos, _ = hdl.allocate_continuations(idx, count, alloc)
+        # trajectories of group g: its 2 roots, then their 7 continuations each;
+        # a continuation trains from its branch position on
+        st = start.view(n_groups, G)
+        st[:, roots_per_group:] = bpos.view(n_groups, -1)
+        adv = hdl.group_advantages(rewards).view(-1)
+        g, _ = hdl.policy_loss_grad(adv, traj, logp_new, logp_old, loss_mask=tmask, pos=pos, start=start,
+                                    scale=1.0 / n_tok)
+        return idx, count, g
+
+    for _ in range(args.warmup):
+        step()
+    torch.cuda.synchronize()
+    stream = torch.cuda.current_stream(dev)
+    ev0 = torch.cuda.Event(enable_timing=True)
+    ev1 = torch.cuda.Event(enable_timing=True)
+    ev0.record(stream)
+    for _ in range(args.steps):
+        idx, count, g = step()
+    ev1.record(stream)
+    torch.cuda.synchronize()
+    step_ms = ev0.elapsed_time(ev1) / args.steps
+    cnt = count.cpu().numpy()
+    log(f"timed {args.steps} group-construction steps: {step_ms:.3f} ms/step "
+        f"({n_groups} groups of {G}, {n_tok} tokens; {cnt.mean():.3f} points per root, "
+        f"{int((cnt < len(alloc)).sum())} roots keep fewer than {len(alloc)})")
+    # the per-token factor pass dominates: 4 (traj) + 4 (pos) + 4 + 4 (log p) + 1 (mask)
+    # bytes read and 8 written per token, plus the per-trajectory reads
+    bytes_tok = 25.0 * n_tok
+    ev2 = torch.cuda.Event(enable_timing=True)
+    ev3 = torch.cuda.Event(enable_timing=True)
+    adv = hdl.group_advantages(rewards).view(-1)
+    ev2.record(stream)
+    for _ in range(args.steps):
+        hdl.policy_loss_grad(adv, traj, logp_new, logp_old, loss_mask=tmask, pos=pos, start=start,
+                             scale=1.0 / n_tok)
+    ev3.record(stream)
+    torch.cuda.synchronize()
+    k_ms = ev2.elapsed_time(ev3) / args.steps
+    achieved = bytes_tok / (k_ms / 1e3) / 1e9
+    result = {
+        "metric": METRIC_GROUP,
+        "value": n_tok / (step_ms / 1e3),
+        "unit": "trained tokens/s",
+        "n_gpus": 1,
+        "steps": args.steps,
+        "warmup": args.warmup,
+        "ms_per_step": step_ms,
+        "higher_is_better": True,
+        "scaling": "weak",
+        "vs_baseline": None,
+        "dtype": "f32",
+        "data": "synthetic (seeded log-probability pairs, rewards and policy log-probabilities)",
+        "config": {"workload": f"{args.workload} trajectory length: {R} roots x T={T}, {n_groups} groups of "
+                               f"{roots_per_group} roots + {G - roots_per_group} continuations (3+4 per root)",
+                   "pass": "group", "min_gap": 64, "index_range": [32, T - 33], "tokens_per_step": n_tok},
+        "roofline": {"bound": "hbm", "achieved": achieved, "peak": 8000.0, "unit": "GB/s",
+                     "frac": achieved / 8000.0, "traffic": None, "kernel": "policy_grad_kernel",
+                     "kernel_ms": k_ms, "bytes_per_launch": bytes_tok},
+    }
+    if not args.no_cpu_baseline:
+        from oracle import hdl_oracle as O
+        t0 = time.perf_counter()
+        sample = 200000
+        sl = slice(0, sample)
+        O.policy_loss_grad(adv.cpu().numpy(), traj[sl].cpu().numpy(), logp_new[sl].cpu().numpy(),
+                           logp_old[sl].cpu().numpy(), tmask[sl].cpu().numpy(), pos[sl].cpu().numpy(),
+                           start.cpu().numpy(), 0.2, 0.28, 1.0 / n_tok)
+        dt = time.perf_counter() - t0
+        result["cpu_baseline"] = {"value": sample / dt, "unit": "trained tokens/s", "cores": 1, "kind": "oracle",
+                                  "sample": f"the oracle's per-token policy-loss factors for the first {sample} "
+                                            f"tokens ({dt:.1f} s; selection and allocation excluded)"}
     print(json.dumps(result), flush=True)
     return 0
 

@@ -198,6 +198,85 @@ int hdl_token_logprobs_backward(const void* hidden, const void* w_vocab, const i
                                 float* grad_hidden, float* grad_w, int accumulate_w,
                                 void* workspace, size_t workspace_bytes, void* stream);
 
+/*
+ * Per-root selection under the branch-point constraints that the paper
+ * applies to every localization method (Sec. 4.3; an allowed index range
+ * and a minimum distance between a root's points, whose values it does not
+ * give, Sec. 4.4 and the Reflection prompt's lo/hi fields).
+ *
+ *  a, b      [n_roots, T] fp32.  b != NULL: rank s = |b - a| (a = logp_orig,
+ *            b = logp_hind, as hdl_select_branch_points).  b == NULL: rank
+ *            a's values themselves (e.g. next-token entropy).
+ *  mask      [n_roots, T] uint8 or NULL.
+ *  lo, hi    [n_roots] int32 or NULL: candidates are positions lo[r] <= t <= hi[r].
+ *  min_gap   retained points of a root are at least min_gap positions apart
+ *            (0 or 1: no spacing constraint).
+ *  refill    0: rank the k best candidates and drop, in rank order, any point
+ *            closer than min_gap to a better retained one (a root may end with
+ *            fewer than k points -- the paper's "only one is retained");
+ *            1: walk down the ranking (at most the best HDL_MAX_K candidates)
+ *            until k points are retained.
+ *  idx, score [n_roots, k], count [n_roots]: retained points in rank order
+ *            (score descending, t ascending), -1 / 0 padding.
+ */
+int hdl_select_constrained(const float* a, const float* b, const uint8_t* mask, int64_t n_roots,
+                           int64_t T, int32_t k, const int32_t* lo, const int32_t* hi,
+                           int32_t min_gap, int refill, int32_t* idx, float* score,
+                           int32_t* count, void* stream);
+
+/*
+ * Continuation slots of each root (Sec. 3.3, Sec. 4.1 "Rollout protocols":
+ * three and four continuations for a root's two branch points; Sec. 4.4:
+ * a root left with one valid point takes all of its continuations there).
+ *
+ *  idx [n_roots, k], count [n_roots]: a selection's output (device).
+ *  alloc        HOST array of k slot counts, in rank order (e.g. {3, 4});
+ *               k <= 16, 1 <= sum <= 4096.
+ *  fallback_pos branch position used when a root has no point at all.
+ *  branch_pos   [n_roots, sum(alloc)] int32 out: the position each
+ *               continuation branches at (it reuses the root's prefix y_<pos).
+ *               Rank j's alloc[j] slots follow rank j-1's; a missing rank's
+ *               slots branch at the root's best point.
+ *  branch_rank  [n_roots, sum(alloc)] int32 out (or NULL): the rank each slot
+ *               branches at, -1 for the fallback.
+ */
+int hdl_allocate_continuations(const int32_t* idx, const int32_t* count, int64_t n_roots,
+                               int32_t k, const int32_t* alloc, int32_t fallback_pos,
+                               int32_t* branch_pos, int32_t* branch_rank, void* stream);
+
+/*
+ * Group-relative advantages without standard-deviation normalisation
+ * (Sec. 3, A_j = R_j - mean(R); Sec. 4.1 follows Dr. GRPO): rewards and adv
+ * are [n_groups, group_size] fp32; one group is a problem's M roots and
+ * G - M continuations.  The mean is a fixed-order fp32 sum.
+ */
+int hdl_group_advantages(const float* rewards, int64_t n_groups, int32_t group_size, float* adv,
+                         void* stream);
+
+/*
+ * Per-token factor g = dL/d log pi of the clipped policy loss (Sec. 4.1
+ * "Training": asymmetric clipping, no KL, token-level aggregation), the
+ * grad_logp input of hdl_token_logprobs_backward:
+ *
+ *     r = exp(logp_new - logp_old),  l = -min(r A, clip(r, 1 - eps_low, 1 + eps_high) A)
+ *     g = scale * dl/dlogp_new = -scale * A r  where the unclipped term is the minimum, else 0
+ *
+ *  adv [n_traj] fp32; traj [n_tokens] int32: each token's trajectory (a
+ *  token whose index is out of [0, n_traj) contributes nothing).
+ *  pos, start (both or neither): pos [n_tokens] int32 is the token's position
+ *  in its trajectory and start [n_traj] int32 the first trained position --
+ *  0 for a root, the branch position for a continuation (only the newly
+ *  sampled suffix is trained, Sec. 3.3).
+ *  loss_mask [n_tokens] uint8 or NULL (policy-generated tokens).
+ *  scale  the aggregation factor, e.g. 1 / (number of trained tokens).
+ *  grad_logp [n_tokens] fp32 out (0 for untrained tokens); loss [n_tokens]
+ *  fp32 out (scale * l, 0 for untrained tokens) or NULL.
+ */
+int hdl_policy_loss_grad(const float* adv, int64_t n_traj, const int32_t* traj, const int32_t* pos,
+                         const int32_t* start, const float* logp_new, const float* logp_old,
+                         const uint8_t* loss_mask, int64_t n_tokens, float eps_low, float eps_high,
+                         float scale, float* grad_logp, float* loss, void* stream);
+
 /* Static description of a status code. */
 const char* hdl_status_string(int status);
 

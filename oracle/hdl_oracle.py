@@ -240,6 +240,113 @@ def select_by_value(values: np.ndarray, mask: Optional[np.ndarray], k: int):
     return idx, score, count
 
 
+# ---------------------------------------------------------------------------
+# Group construction (Sec. 3.3, Sec. 4.1, Sec. 4.3-4.4)
+# ---------------------------------------------------------------------------
+def select_constrained(a: np.ndarray, b: Optional[np.ndarray], mask: Optional[np.ndarray], k: int,
+                       lo=None, hi=None, min_gap: int = 0, refill: bool = False,
+                       precision: str = "f64", pool_cap: int = 1024):
+    """Per-root selection under the branch-point constraints.
+
+    Score: |b - a| (Eq. 2; `precision="f32"` evaluates the difference as one
+    binary32 subtraction) or, with b None, a's values.  Candidates: mask != 0,
+    finite score, lo[r] <= t <= hi[r].  Ranked by (score desc, t asc).  A
+    point is retained if it lies at least min_gap from every point retained
+    before it (min_gap <= 1: always); without refill only the top k ranked
+    candidates are considered (so fewer than k may remain), with refill the
+    best `pool_cap` candidates are walked until k are retained.
+    """
+    a = np.asarray(a)
+    R, T = a.shape
+    if b is None:
+        sc = a.astype(np.float64)
+    elif precision == "f32":
+        sc = np.abs((np.asarray(b, np.float32) - np.asarray(a, np.float32)).astype(np.float64))
+    else:
+        sc = np.abs(np.asarray(b, np.float64) - a.astype(np.float64))
+    m = np.ones((R, T), bool) if mask is None else (np.asarray(mask) != 0)
+    idx = np.full((R, k), -1, dtype=np.int32)
+    score = np.zeros((R, k), dtype=np.float64)
+    count = np.zeros(R, dtype=np.int32)
+    for r in range(R):
+        t_lo = 0 if lo is None else int(lo[r])
+        t_hi = T - 1 if hi is None else int(hi[r])
+        cand = [t for t in range(T) if m[r, t] and np.isfinite(sc[r, t]) and t_lo <= t <= t_hi]
+        ranked = sorted(cand, key=lambda t: (-sc[r, t], t))
+        pool = ranked[:pool_cap] if refill else ranked[:k]
+        kept = []
+        for t in pool:
+            if len(kept) == k:
+                break
+            if min_gap <= 1 or all(abs(t - u) >= min_gap for u in kept):
+                kept.append(t)
+        count[r] = len(kept)
+        for j, t in enumerate(kept):
+            idx[r, j] = t
+            score[r, j] = sc[r, t]
+    return idx, score, count
+
+
+def allocate_continuations(idx: np.ndarray, count: np.ndarray, alloc, fallback: int = 0):
+    """Branch position (and rank, -1 for the fallback) of every continuation
+    slot: rank j takes alloc[j] slots in rank order; a rank the root does not
+    have sends its slots to the root's best point (Sec. 4.4: a root with one
+    valid point takes all of its continuations there); a root with no point
+    branches at `fallback`."""
+    idx = np.asarray(idx)
+    R, k = idx.shape
+    total = int(sum(alloc))
+    pos = np.zeros((R, total), dtype=np.int32)
+    rank = np.zeros((R, total), dtype=np.int32)
+    for r in range(R):
+        c = max(0, min(int(count[r]), k))
+        slot = 0
+        for j in range(k):
+            for _ in range(int(alloc[j])):
+                if c == 0:
+                    pos[r, slot], rank[r, slot] = fallback, -1
+                else:
+                    target = j if j < c else 0
+                    pos[r, slot], rank[r, slot] = idx[r, target], target
+                slot += 1
+    return pos, rank
+
+
+def group_advantages(rewards: np.ndarray) -> np.ndarray:
+    """A_j = R_j - mean_k R_k within each group (row); no std normalisation
+    (Sec. 3; Sec. 4.1 follows Dr. GRPO)."""
+    R = np.asarray(rewards, dtype=np.float64)
+    return R - R.mean(axis=1, keepdims=True)
+
+
+def policy_loss_grad(adv, traj, logp_new, logp_old, loss_mask=None, pos=None, start=None,
+                     eps_low: float = 0.2, eps_high: float = 0.28, scale: float = 1.0):
+    """Per-token loss l = -scale * min(r A, clip(r, 1 - eps_low, 1 + eps_high) A)
+    with r = exp(logp_new - logp_old), and g = dl/dlogp_new (Sec. 4.1
+    "Training"); tokens outside the loss mask, before their trajectory's
+    first trained position (a continuation's reused prefix, Sec. 3.3) or
+    with an out-of-range trajectory index give 0.  Returns (g, l)."""
+    adv = np.asarray(adv, dtype=np.float64)
+    traj = np.asarray(traj).astype(np.int64)
+    n = traj.shape[0]
+    g = np.zeros(n)
+    loss = np.zeros(n)
+    for i in range(n):
+        j = traj[i]
+        on = 0 <= j < adv.shape[0] and (loss_mask is None or loss_mask[i] != 0)
+        if on and pos is not None:
+            on = pos[i] >= start[j]
+        if not on:
+            continue
+        r = math.exp(float(logp_new[i]) - float(logp_old[i]))
+        a = adv[j]
+        rc = min(max(r, 1.0 - eps_low), 1.0 + eps_high)
+        unclipped, clipped = r * a, rc * a
+        loss[i] = -scale * min(unclipped, clipped)
+        g[i] = -scale * a * r if unclipped <= clipped else 0.0
+    return g, loss
+
+
 def branch_set_agrees(gpu_idx, gpu_count, oracle_scores, eligible, k,
                       gap: float = 1e-2) -> Tuple[bool, str]:
     """Acceptance rule for one root when several answers can be right.

@@ -19,7 +19,8 @@ import torch
 
 __all__ = ["HdlError", "HDL_F32", "HDL_BF16", "HDL_MAX_K", "library_path", "load_library",
            "workspace_size", "token_logprobs", "token_logprobs_backward", "select_branch_points",
-           "select_top_k", "rescore",
+           "select_top_k", "select_constrained", "allocate_continuations", "group_advantages",
+           "policy_loss_grad", "rescore",
            "profile_enable", "profile_read", "abi_version"]
 
 HDL_F32 = 0
@@ -65,6 +66,17 @@ def load_library() -> ctypes.CDLL:
     L.hdl_token_logprobs_backward.argtypes = [c_vp, c_vp, c_vp, c_vp, c_vp, c_vp, c_i64, c_i64, c_i64,
                                               ctypes.c_int, c_vp, c_vp, ctypes.c_int, c_vp, c_sz, c_vp]
     L.hdl_token_logprobs_backward.restype = ctypes.c_int
+    L.hdl_select_constrained.argtypes = [c_vp, c_vp, c_vp, c_i64, c_i64, ctypes.c_int32, c_vp, c_vp,
+                                         ctypes.c_int32, ctypes.c_int, c_vp, c_vp, c_vp, c_vp]
+    L.hdl_select_constrained.restype = ctypes.c_int
+    L.hdl_allocate_continuations.argtypes = [c_vp, c_vp, c_i64, ctypes.c_int32, c_vp, ctypes.c_int32, c_vp,
+                                             c_vp, c_vp]
+    L.hdl_allocate_continuations.restype = ctypes.c_int
+    L.hdl_group_advantages.argtypes = [c_vp, c_i64, ctypes.c_int32, c_vp, c_vp]
+    L.hdl_group_advantages.restype = ctypes.c_int
+    L.hdl_policy_loss_grad.argtypes = [c_vp, c_i64, c_vp, c_vp, c_vp, c_vp, c_vp, c_vp, c_i64, ctypes.c_float,
+                                       ctypes.c_float, ctypes.c_float, c_vp, c_vp, c_vp]
+    L.hdl_policy_loss_grad.restype = ctypes.c_int
     L.hdl_select_branch_points.argtypes = [c_vp, c_vp, c_vp, c_i64, c_i64, ctypes.c_int32,
                                            c_vp, c_vp, c_vp, c_vp, c_vp]
     L.hdl_select_branch_points.restype = ctypes.c_int
@@ -290,6 +302,104 @@ def token_logprobs_backward(hidden: torch.Tensor, w_vocab: torch.Tensor, tokens:
 
 def backward_workspace_size(n_rows: int, d: int, vocab: int) -> int:
     return int(load_library().hdl_token_logprobs_backward_workspace_size(n_rows, d, vocab, HDL_BF16))
+
+
+def _dev_2d(name, t, dtype, shape=None):
+    _require_cuda(name, t)
+    if t.dtype != dtype or (shape is not None and tuple(t.shape) != tuple(shape)):
+        raise ValueError(f"{name} must be {dtype} {list(shape) if shape else ''}")
+    return t
+
+
+def select_constrained(a: torch.Tensor, b: Optional[torch.Tensor], mask: Optional[torch.Tensor], k: int, *,
+                       lo: Optional[torch.Tensor] = None, hi: Optional[torch.Tensor] = None, min_gap: int = 0,
+                       refill: bool = False):
+    """Per-root top-k under the branch-point constraints (index range
+    [lo, hi] per root, minimum spacing).  b given: rank |b - a| (Eq. 2);
+    b None: rank a's values.  Returns (idx [R,k], score [R,k], count [R])."""
+    L = load_library()
+    _dev_2d("a", a, torch.float32)
+    if a.dim() != 2:
+        raise ValueError("a must be [R, T]")
+    R, T = a.shape
+    if b is not None:
+        _dev_2d("b", b, torch.float32, (R, T))
+    if mask is not None:
+        if mask.dtype == torch.bool:
+            mask = mask.view(torch.uint8)
+        _dev_2d("mask", mask, torch.uint8, (R, T))
+    for name, t in (("lo", lo), ("hi", hi)):
+        if t is not None:
+            _dev_2d(name, t, torch.int32, (R,))
+    dev = a.device
+    kk = max(int(k), 1)
+    idx = torch.empty(R, kk, dtype=torch.int32, device=dev)
+    score = torch.empty(R, kk, dtype=torch.float32, device=dev)
+    count = torch.empty(R, dtype=torch.int32, device=dev)
+    _check(L.hdl_select_constrained(a.data_ptr(), _ptr(b), _ptr(mask), R, T, int(k), _ptr(lo), _ptr(hi),
+                                    int(min_gap), 1 if refill else 0, idx.data_ptr(), score.data_ptr(),
+                                    count.data_ptr(), _stream_handle(dev)))
+    return idx, score, count
+
+
+def allocate_continuations(idx: torch.Tensor, count: torch.Tensor, alloc=(3, 4), fallback_pos: int = 0):
+    """Continuation slots per root: returns (branch_pos [R, sum(alloc)], branch_rank [R, sum(alloc)])."""
+    L = load_library()
+    _dev_2d("idx", idx, torch.int32)
+    R, k = idx.shape
+    _dev_2d("count", count, torch.int32, (R,))
+    if len(alloc) != k:
+        raise ValueError("alloc needs one entry per selected rank")
+    total = int(sum(alloc))
+    host = (ctypes.c_int32 * k)(*[int(x) for x in alloc])
+    pos = torch.empty(R, max(total, 1), dtype=torch.int32, device=idx.device)
+    rank = torch.empty_like(pos)
+    _check(L.hdl_allocate_continuations(idx.data_ptr(), count.data_ptr(), R, k, ctypes.addressof(host),
+                                        int(fallback_pos), pos.data_ptr(), rank.data_ptr(),
+                                        _stream_handle(idx.device)))
+    return pos, rank
+
+
+def group_advantages(rewards: torch.Tensor) -> torch.Tensor:
+    """A = R - mean over each group (rows of rewards [n_groups, G], fp32)."""
+    L = load_library()
+    _dev_2d("rewards", rewards, torch.float32)
+    n, G = rewards.shape
+    adv = torch.empty_like(rewards)
+    _check(L.hdl_group_advantages(rewards.data_ptr(), n, G, adv.data_ptr(), _stream_handle(rewards.device)))
+    return adv
+
+
+def policy_loss_grad(adv: torch.Tensor, traj: torch.Tensor, logp_new: torch.Tensor, logp_old: torch.Tensor, *,
+                     loss_mask: Optional[torch.Tensor] = None, pos: Optional[torch.Tensor] = None,
+                     start: Optional[torch.Tensor] = None, eps_low: float = 0.2, eps_high: float = 0.28,
+                     scale: Optional[float] = None):
+    """Per-token g = dL/dlog pi of the clipped token-level policy loss and the
+    per-token loss; scale defaults to 1 / (number of tokens in the mask)."""
+    L = load_library()
+    _dev_2d("adv", adv, torch.float32)
+    n = traj.numel()
+    _dev_2d("traj", traj, torch.int32, (n,))
+    _dev_2d("logp_new", logp_new, torch.float32, (n,))
+    _dev_2d("logp_old", logp_old, torch.float32, (n,))
+    if loss_mask is not None:
+        if loss_mask.dtype == torch.bool:
+            loss_mask = loss_mask.view(torch.uint8)
+        _dev_2d("loss_mask", loss_mask, torch.uint8, (n,))
+    if (pos is None) != (start is None):
+        raise ValueError("pos and start go together")
+    if pos is not None:
+        _dev_2d("pos", pos, torch.int32, (n,))
+        _dev_2d("start", start, torch.int32, (adv.numel(),))
+    if scale is None:
+        scale = 1.0 / max(1, int(n if loss_mask is None else loss_mask.sum().item()))
+    grad = torch.empty(n, dtype=torch.float32, device=traj.device)
+    loss = torch.empty_like(grad)
+    _check(L.hdl_policy_loss_grad(adv.data_ptr(), adv.numel(), traj.data_ptr(), _ptr(pos), _ptr(start),
+                                  logp_new.data_ptr(), logp_old.data_ptr(), _ptr(loss_mask), n, float(eps_low),
+                                  float(eps_high), float(scale), grad.data_ptr(), loss.data_ptr(),
+                                  _stream_handle(traj.device)))
+    return grad, loss
 
 
 def rescore(hidden_both: torch.Tensor, w_vocab: torch.Tensor, tokens: torch.Tensor,

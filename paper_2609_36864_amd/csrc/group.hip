@@ -1,0 +1,131 @@
+// Localized group construction and the group-relative policy-loss factors
+// (Sec. 3.3 and Sec. 4.1):
+//
+//  * allocate_kernel: each root's continuation slots are assigned to its
+//    retained branch points in rank order (the default 3 + 4 for two points
+//    per root); slots of a point that was not retained go to the root's best
+//    point, so a root with one valid point still fills all of its slots; a
+//    root with none branches at a fallback position.
+//  * advantages_kernel: the mean-centred group advantage A_j = R_j - mean(R)
+//    without standard-deviation normalisation.
+//  * policy_grad_kernel: per token, the derivative of the asymmetrically
+//    clipped surrogate -min(r A, clip(r, 1 - eps_low, 1 + eps_high) A) with
+//    respect to log pi (r = pi / pi_old), times the token-level aggregation
+//    factor; tokens before their trajectory's branch point (the reused
+//    prefix of a continuation) and tokens outside the loss mask contribute
+//    nothing.  The result is the per-token g that the lm-head backward pass
+//    takes.
+#include "hdl_internal.h"
+
+namespace hdl {
+namespace {
+
+constexpr int kMaxAlloc = 16;
+
+struct Alloc {
+  int32_t n[kMaxAlloc];
+};
+
+__global__ __launch_bounds__(256) void allocate_kernel(const int32_t* __restrict__ idx,
+                                                       const int32_t* __restrict__ count, int64_t n_roots,
+                                                       int k, Alloc alloc, int total, int32_t fallback,
+                                                       int32_t* __restrict__ branch_pos,
+                                                       int32_t* __restrict__ branch_rank) {
+  const int64_t r = static_cast<int64_t>(blockIdx.x) * blockDim.x + threadIdx.x;
+  if (r >= n_roots) return;
+  int c = count[r];
+  c = c < 0 ? 0 : (c > k ? k : c);
+  int32_t* pos = branch_pos + r * total;
+  int32_t* rnk = branch_rank ? branch_rank + r * total : nullptr;
+  int slot = 0;
+  for (int j = 0; j < k; ++j) {
+    const int target = j < c ? j : 0;
+    const int32_t p = c > 0 ? idx[r * k + target] : fallback;
+    for (int u = 0; u < alloc.n[j]; ++u, ++slot) {
+      pos[slot] = p;
+      if (rnk) rnk[slot] = c > 0 ? target : -1;
+    }
+  }
+}
+
+// One workgroup per group; the mean is a fixed-order tree sum.
+__global__ __launch_bounds__(256) void advantages_kernel(const float* __restrict__ rewards, int group_size,
+                                                         float* __restrict__ adv) {
+  __shared__ float part[256];
+  const int64_t g = blockIdx.x;
+  const float* R = rewards + g * group_size;
+  float s = 0.f;
+  for (int j = threadIdx.x; j < group_size; j += 256) s += R[j];
+  part[threadIdx.x] = s;
+  __syncthreads();
+  for (int w = 128; w > 0; w >>= 1) {
+    if (threadIdx.x < w) part[threadIdx.x] += part[threadIdx.x + w];
+    __syncthreads();
+  }
+  const float mean = part[0] / static_cast<float>(group_size);
+  for (int j = threadIdx.x; j < group_size; j += 256) adv[g * group_size + j] = R[j] - mean;
+}
+
+__global__ __launch_bounds__(256) void policy_grad_kernel(const float* __restrict__ adv,
+                                                          const int32_t* __restrict__ traj,
+                                                          const int32_t* __restrict__ pos,
+                                                          const int32_t* __restrict__ start,
+                                                          const float* __restrict__ logp_new,
+                                                          const float* __restrict__ logp_old,
+                                                          const uint8_t* __restrict__ loss_mask,
+                                                          int64_t n_tokens, int64_t n_traj, float eps_low,
+                                                          float eps_high,
+                                                          float scale, float* __restrict__ grad,
+                                                          float* __restrict__ loss) {
+  const int64_t n = static_cast<int64_t>(blockIdx.x) * blockDim.x + threadIdx.x;
+  if (n >= n_tokens) return;
+  const int32_t j = traj[n];
+  bool on = (loss_mask == nullptr || loss_mask[n] != 0) && j >= 0 && j < n_traj;
+  if (pos && start) on = on && pos[n] >= start[j];
+  float gv = 0.f, lv = 0.f;
+  if (on) {
+    const float a = adv[j];
+    const float r = expf(logp_new[n] - logp_old[n]);
+    const float rc = fminf(fmaxf(r, 1.f - eps_low), 1.f + eps_high);
+    const float unclipped = r * a, clipped = rc * a;
+    // d/dlog pi of min(r A, clip(r) A): r A where the unclipped term is the
+    // minimum (ties included), 0 where the clipped constant is
+    gv = unclipped <= clipped ? -a * r * scale : 0.f;
+    lv = -fminf(unclipped, clipped) * scale;
+  }
+  grad[n] = gv;
+  if (loss) loss[n] = lv;
+}
+
+}  // namespace
+
+hipError_t launch_allocate(const int32_t* idx, const int32_t* count, int64_t n_roots, int k,
+                           const int32_t* alloc, int total, int32_t fallback, int32_t* branch_pos,
+                           int32_t* branch_rank, hipStream_t stream) {
+  Alloc a{};
+  for (int j = 0; j < k && j < kMaxAlloc; ++j) a.n[j] = alloc[j];
+  const int64_t blocks = (n_roots + 255) / 256;
+  hipLaunchKernelGGL(allocate_kernel, dim3(static_cast<unsigned>(blocks)), dim3(256), 0, stream, idx, count,
+                     n_roots, k, a, total, fallback, branch_pos, branch_rank);
+  return hipGetLastError();
+}
+
+hipError_t launch_advantages(const float* rewards, int64_t n_groups, int group_size, float* adv,
+                             hipStream_t stream) {
+  hipLaunchKernelGGL(advantages_kernel, dim3(static_cast<unsigned>(n_groups)), dim3(256), 0, stream, rewards,
+                     group_size, adv);
+  return hipGetLastError();
+}
+
+hipError_t launch_policy_grad(const float* adv, const int32_t* traj, const int32_t* pos, const int32_t* start,
+                              const float* logp_new, const float* logp_old, const uint8_t* loss_mask,
+                              int64_t n_tokens, int64_t n_traj, float eps_low, float eps_high, float scale,
+                              float* grad, float* loss, hipStream_t stream) {
+  const int64_t blocks = (n_tokens + 255) / 256;
+  hipLaunchKernelGGL(policy_grad_kernel, dim3(static_cast<unsigned>(blocks)), dim3(256), 0, stream, adv, traj,
+                     pos, start, logp_new, logp_old, loss_mask, n_tokens, n_traj, eps_low, eps_high, scale, grad,
+                     loss);
+  return hipGetLastError();
+}
+
+}  // namespace hdl

@@ -272,7 +272,7 @@ const char* hdl_status_string(int status) {
 
 const char* hdl_last_error(void) { return g_last_error; }
 
-int hdl_abi_version(void) { return 3; }
+int hdl_abi_version(void) { return 4; }
 
 int hdl_profile_enable(int on) {
   std::lock_guard<std::mutex> lk(g_prof.mu);
@@ -502,6 +502,83 @@ int hdl_token_logprobs_backward(const void* hidden, const void* w_vocab, const i
     gw.beta = (c > 0 || accumulate_w) ? 1 : 0;
     if ((e = hdl::launch_gemm_nt(gw, s)) != hipSuccess) return hip_fail(e, "GEMM launch");
   }
+  return HDL_OK;
+}
+
+}  // extern "C"
+
+// ---- branch-point constraints and group construction ---------------------
+extern "C" {
+
+int hdl_select_constrained(const float* a, const float* b, const uint8_t* mask, int64_t n_roots, int64_t T,
+                           int32_t k, const int32_t* lo, const int32_t* hi, int32_t min_gap, int refill,
+                           int32_t* idx, float* score, int32_t* count, void* stream) {
+  const char* fn = "hdl_select_constrained";
+  g_last_error[0] = '\0';
+  if (!a || !idx || !score || !count) return fail(HDL_ERR_INVALID_ARG, "%s: null required pointer", fn);
+  if (n_roots <= 0 || T <= 0) return fail(HDL_ERR_INVALID_ARG, "%s: n_roots and T must be positive", fn);
+  if (k < 1) return fail(HDL_ERR_INVALID_ARG, "%s: k=%d must be >= 1", fn, k);
+  if (k > HDL_MAX_K) return fail(HDL_ERR_UNSUPPORTED, "%s: k=%d exceeds %d", fn, k, HDL_MAX_K);
+  if (n_roots > INT32_MAX || T > INT32_MAX)
+    return fail(HDL_ERR_UNSUPPORTED, "%s: n_roots and T must fit in int32", fn);
+  if (min_gap < 0) return fail(HDL_ERR_INVALID_ARG, "%s: min_gap=%d must be >= 0", fn, min_gap);
+  const int pool = refill ? HDL_MAX_K : k;
+  hipError_t e = hdl::launch_select(a, b, mask, n_roots, T, k, idx, score, count, nullptr, b == nullptr,
+                                    static_cast<hipStream_t>(stream), lo, hi, min_gap, pool);
+  if (e != hipSuccess) return hip_fail(e, "selection kernel launch");
+  return HDL_OK;
+}
+
+int hdl_allocate_continuations(const int32_t* idx, const int32_t* count, int64_t n_roots, int32_t k,
+                               const int32_t* alloc, int32_t fallback_pos, int32_t* branch_pos,
+                               int32_t* branch_rank, void* stream) {
+  const char* fn = "hdl_allocate_continuations";
+  g_last_error[0] = '\0';
+  if (!idx || !count || !alloc || !branch_pos) return fail(HDL_ERR_INVALID_ARG, "%s: null required pointer", fn);
+  if (n_roots <= 0 || k < 1) return fail(HDL_ERR_INVALID_ARG, "%s: n_roots and k must be positive", fn);
+  if (k > 16) return fail(HDL_ERR_UNSUPPORTED, "%s: k=%d exceeds 16 branch points per root", fn, k);
+  if (n_roots > INT32_MAX) return fail(HDL_ERR_UNSUPPORTED, "%s: n_roots must fit in int32", fn);
+  int64_t total = 0;
+  for (int j = 0; j < k; ++j) {
+    if (alloc[j] < 0) return fail(HDL_ERR_INVALID_ARG, "%s: alloc[%d]=%d is negative", fn, j, alloc[j]);
+    total += alloc[j];
+  }
+  if (total < 1 || total > 4096)
+    return fail(HDL_ERR_INVALID_ARG, "%s: %lld continuations per root (1 .. 4096)", fn, static_cast<long long>(total));
+  hipError_t e = hdl::launch_allocate(idx, count, n_roots, k, alloc, static_cast<int>(total), fallback_pos,
+                                      branch_pos, branch_rank, static_cast<hipStream_t>(stream));
+  if (e != hipSuccess) return hip_fail(e, "allocation kernel launch");
+  return HDL_OK;
+}
+
+int hdl_group_advantages(const float* rewards, int64_t n_groups, int32_t group_size, float* adv, void* stream) {
+  const char* fn = "hdl_group_advantages";
+  g_last_error[0] = '\0';
+  if (!rewards || !adv) return fail(HDL_ERR_INVALID_ARG, "%s: null required pointer", fn);
+  if (n_groups <= 0 || group_size <= 0)
+    return fail(HDL_ERR_INVALID_ARG, "%s: n_groups and group_size must be positive", fn);
+  if (n_groups > INT32_MAX) return fail(HDL_ERR_UNSUPPORTED, "%s: n_groups must fit in int32", fn);
+  hipError_t e = hdl::launch_advantages(rewards, n_groups, group_size, adv, static_cast<hipStream_t>(stream));
+  if (e != hipSuccess) return hip_fail(e, "advantage kernel launch");
+  return HDL_OK;
+}
+
+int hdl_policy_loss_grad(const float* adv, int64_t n_traj, const int32_t* traj, const int32_t* pos,
+                         const int32_t* start, const float* logp_new, const float* logp_old,
+                         const uint8_t* loss_mask, int64_t n_tokens, float eps_low, float eps_high, float scale,
+                         float* grad_logp, float* loss, void* stream) {
+  const char* fn = "hdl_policy_loss_grad";
+  g_last_error[0] = '\0';
+  if (!adv || !traj || !logp_new || !logp_old || !grad_logp)
+    return fail(HDL_ERR_INVALID_ARG, "%s: null required pointer", fn);
+  if ((pos == nullptr) != (start == nullptr))
+    return fail(HDL_ERR_INVALID_ARG, "%s: pos and start must be given together", fn);
+  if (n_traj <= 0 || n_tokens <= 0) return fail(HDL_ERR_INVALID_ARG, "%s: sizes must be positive", fn);
+  if (n_tokens > (int64_t{1} << 38)) return fail(HDL_ERR_UNSUPPORTED, "%s: too many tokens", fn);
+  if (!(eps_low >= 0.f) || !(eps_high >= 0.f)) return fail(HDL_ERR_INVALID_ARG, "%s: negative clip range", fn);
+  hipError_t e = hdl::launch_policy_grad(adv, traj, pos, start, logp_new, logp_old, loss_mask, n_tokens, n_traj,
+                                         eps_low, eps_high, scale, grad_logp, loss, static_cast<hipStream_t>(stream));
+  if (e != hipSuccess) return hip_fail(e, "policy-gradient kernel launch");
   return HDL_OK;
 }
 

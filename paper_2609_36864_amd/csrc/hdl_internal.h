@@ -120,6 +120,18 @@ hipError_t launch_merge(const LmheadArgs& a, int64_t n_rows, float* logp, float*
 // values == true: rank `lo` itself (lh unused); otherwise rank |lh - lo|.
 hipError_t launch_select(const float* lo, const float* lh, const uint8_t* mask,
                          int64_t n_roots, int64_t T, int k, int32_t* idx, float* score,
-                         int32_t* count, float* delta, bool values, hipStream_t stream);
+                         int32_t* count, float* delta, bool values, hipStream_t stream,
+                         const int32_t* r_lo = nullptr, const int32_t* r_hi = nullptr, int min_gap = 0,
+                         int pool = 0);
+// Group construction (group.hip).
+hipError_t launch_allocate(const int32_t* idx, const int32_t* count, int64_t n_roots, int k,
+                           const int32_t* alloc, int total, int32_t fallback, int32_t* branch_pos,
+                           int32_t* branch_rank, hipStream_t stream);
+hipError_t launch_advantages(const float* rewards, int64_t n_groups, int group_size, float* adv,
+                             hipStream_t stream);
+hipError_t launch_policy_grad(const float* adv, const int32_t* traj, const int32_t* pos, const int32_t* start,
+                              const float* logp_new, const float* logp_old, const uint8_t* loss_mask,
+                              int64_t n_tokens, int64_t n_traj, float eps_low, float eps_high, float scale,
+                              float* grad, float* loss, hipStream_t stream);
 
 }  // namespace hdl

@@ -15,6 +15,15 @@
 // are the lowest-indexed ties (a scan in position order).  The kk <= 1024
 // winners are then sorted by the composite key (s, ~t) with a bitonic sort
 // in LDS, giving the order (s descending, t ascending).
+//
+// Branch-point constraints (the paper applies the same ones to every
+// localization method, Sec. 4.3): candidates may be restricted to a per-root
+// index range [lo, hi], and retained points must lie at least min_gap
+// positions apart.  The spacing filter walks the ranked winners and keeps a
+// point only if it is far enough from every point kept before it; without
+// refill the walk sees only the top k (a point too close to a better one is
+// dropped, so a root can end with fewer than k points), with refill it sees
+// up to the best 1024 candidates and keeps going until k points are kept.
 #include "hdl_internal.h"
 
 namespace hdl {
@@ -29,6 +38,7 @@ struct Scratch {
   int digit;
   int rank;
   unsigned long long keys[kThreads];
+  int kept;
 };
 
 __device__ __forceinline__ int wave_incl_scan(int v) {
@@ -89,6 +99,16 @@ __device__ __forceinline__ Pos load_pos(const float* lo, const float* lh, const 
   return p;
 }
 
+// Candidate for ranking: eligible and inside the root's index range.
+__device__ __forceinline__ Pos load_cand(bool values, const float* lo, const float* lh, const uint8_t* mask,
+                                         int64_t base, int64_t t, int64_t t_lo, int64_t t_hi) {
+  Pos p = values ? load_pos<true>(lo, lh, mask, base, t) : load_pos<false>(lo, lh, mask, base, t);
+  p.elig = p.elig && t >= t_lo && t <= t_hi;
+  return p;
+}
+
+// pool: winners ranked before the spacing filter (k without refill);
+// min_gap <= 1 disables the filter; r_lo / r_hi (optional) bound the range.
 template <bool VALUES>
 __global__ __launch_bounds__(kThreads) void select_kernel(const float* __restrict__ lo,
                                                           const float* __restrict__ lh,
@@ -97,22 +117,27 @@ __global__ __launch_bounds__(kThreads) void select_kernel(const float* __restric
                                                           int32_t* __restrict__ idx,
                                                           float* __restrict__ score,
                                                           int32_t* __restrict__ count,
-                                                          float* __restrict__ delta_out) {
+                                                          float* __restrict__ delta_out,
+                                                          const int32_t* __restrict__ r_lo,
+                                                          const int32_t* __restrict__ r_hi,
+                                                          int min_gap, int pool) {
   __shared__ Scratch sh;
   const int r = blockIdx.x;
   const int tid = threadIdx.x;
   const int64_t base = static_cast<int64_t>(r) * T;
+  const int64_t t_lo = r_lo ? r_lo[r] : 0;
+  const int64_t t_hi = r_hi ? r_hi[r] : T - 1;
 
   // ---- eligibility count (and the optional signed delta) -----------------
   int c = 0;
   for (int64_t t = tid; t < T; t += kThreads) {
     const Pos p = load_pos<VALUES>(lo, lh, mask, base, t);
     if (delta_out) delta_out[base + t] = p.delta;
-    c += p.elig ? 1 : 0;
+    c += (p.elig && t >= t_lo && t <= t_hi) ? 1 : 0;
   }
   int n_elig;
   block_excl_scan(c, &n_elig, sh);
-  const int kk = n_elig < k ? n_elig : k;
+  const int kk = n_elig < pool ? n_elig : pool;
 
   if (kk > 0) {
     // ---- radix select of the kk-th largest score --------------------------
@@ -122,7 +147,7 @@ __global__ __launch_bounds__(kThreads) void select_kernel(const float* __restric
       for (int i = tid; i < 256; i += kThreads) sh.hist[i] = 0;
       __syncthreads();
       for (int64_t t = tid; t < T; t += kThreads) {
-        const Pos p = load_pos<VALUES>(lo, lh, mask, base, t);
+        const Pos p = load_cand(VALUES, lo, lh, mask, base, t, t_lo, t_hi);
         if (p.elig && (p.key & pmask) == prefix) atomicAdd(&sh.hist[(p.key >> shift) & 255], 1);
       }
       __syncthreads();
@@ -149,7 +174,7 @@ __global__ __launch_bounds__(kThreads) void select_kernel(const float* __restric
     for (int64_t t0 = 0; t0 < T; t0 += kThreads) {
       const int64_t t = t0 + tid;
       Pos p;
-      if (t < T) p = load_pos<VALUES>(lo, lh, mask, base, t);
+      if (t < T) p = load_cand(VALUES, lo, lh, mask, base, t, t_lo, t_hi);
       else { p.elig = false; p.key = 0; p.delta = 0.f; }
       const bool eq = p.elig && p.key == thr;
       int n_eq;
@@ -190,8 +215,29 @@ __global__ __launch_bounds__(kThreads) void select_kernel(const float* __restric
     }
   }
 
+  // ---- spacing filter over the ranked winners ----------------------------
+  int n_out = kk < k ? kk : k;
+  if (min_gap > 1 && kk > 0) {
+    if (tid == 0) {
+      int kept = 0;
+      for (int j = 0; j < kk && kept < k; ++j) {
+        const unsigned long long key = sh.keys[j];
+        const int64_t t = 0xFFFFFFFFu - static_cast<unsigned>(key & 0xFFFFFFFFull);
+        bool ok = true;
+        for (int q = 0; q < kept && ok; ++q) {
+          const int64_t u = 0xFFFFFFFFu - static_cast<unsigned>(sh.keys[q] & 0xFFFFFFFFull);
+          ok = (t > u ? t - u : u - t) >= min_gap;
+        }
+        if (ok) sh.keys[kept++] = key;   // kept <= j: compaction in place
+      }
+      sh.kept = kept;
+    }
+    __syncthreads();
+    n_out = sh.kept;
+  }
+
   for (int j = tid; j < k; j += kThreads) {
-    if (j < kk) {
+    if (j < n_out) {
       const unsigned long long key = sh.keys[j];
       idx[static_cast<int64_t>(r) * k + j] = static_cast<int32_t>(0xFFFFFFFFu - static_cast<unsigned>(key & 0xFFFFFFFFull));
       score[static_cast<int64_t>(r) * k + j] = key_float(static_cast<unsigned>(key >> 32));
@@ -200,20 +246,22 @@ __global__ __launch_bounds__(kThreads) void select_kernel(const float* __restric
       score[static_cast<int64_t>(r) * k + j] = 0.f;
     }
   }
-  if (tid == 0) count[r] = kk;
+  if (tid == 0) count[r] = n_out;
 }
 
 }  // namespace
 
 hipError_t launch_select(const float* lo, const float* lh, const uint8_t* mask, int64_t n_roots,
                          int64_t T, int k, int32_t* idx, float* score, int32_t* count, float* delta,
-                         bool values, hipStream_t stream) {
+                         bool values, hipStream_t stream, const int32_t* r_lo, const int32_t* r_hi,
+                         int min_gap, int pool) {
+  if (pool < k) pool = k;
   if (values)
     hipLaunchKernelGGL(select_kernel<true>, dim3(static_cast<unsigned>(n_roots)), dim3(kThreads), 0,
-                       stream, lo, lh, mask, T, k, idx, score, count, delta);
+                       stream, lo, lh, mask, T, k, idx, score, count, delta, r_lo, r_hi, min_gap, pool);
   else
     hipLaunchKernelGGL(select_kernel<false>, dim3(static_cast<unsigned>(n_roots)), dim3(kThreads), 0,
-                       stream, lo, lh, mask, T, k, idx, score, count, delta);
+                       stream, lo, lh, mask, T, k, idx, score, count, delta, r_lo, r_hi, min_gap, pool);
   return hipGetLastError();
 }
 

@@ -30,7 +30,9 @@ def test_header_declares_the_boundary():
     names = _declared_functions()
     for n in ("hdl_token_logprobs", "hdl_token_logprobs_entropy", "hdl_select_branch_points",
               "hdl_select_top_k", "hdl_token_logprobs_workspace_size", "hdl_status_string",
-              "hdl_last_error", "hdl_token_logprobs_backward", "hdl_token_logprobs_backward_workspace_size"):
+              "hdl_last_error", "hdl_token_logprobs_backward", "hdl_token_logprobs_backward_workspace_size",
+              "hdl_select_constrained", "hdl_allocate_continuations", "hdl_group_advantages",
+              "hdl_policy_loss_grad"):
         assert n in names
 
 
@@ -43,7 +45,7 @@ def test_status_strings(lib):
     assert lib.hdl_status_string(0) == b"ok"
     for s in (-1, -2, -3, -4):
         assert lib.hdl_status_string(s) not in (b"ok", b"unknown status")
-    assert lib.hdl_abi_version() == 3
+    assert lib.hdl_abi_version() == 4
 
 
 def test_workspace_size_rules(lib):
@@ -113,3 +115,35 @@ def test_backward_workspace_and_argument_errors(lib):
     assert f(p, p, p, None, p, p, n, d, V, 0, p, p, 0, p, size, None) == -2      # fp32
     assert f(p, p, p, None, p, p, n, d, V, 1, p, p, 0, p, size - 256, None) == -3
     assert f(p, p, p, None, p, p, n, d, V, 1, p, p, 0, ctypes.c_void_p(4096 + 16), size, None) == -1
+
+
+def test_group_construction_argument_errors(lib):
+    p = ctypes.c_void_p(4096)
+    sc = lib.hdl_select_constrained
+    sc.restype = ctypes.c_int
+    sc.argtypes = [ctypes.c_void_p] * 3 + [ctypes.c_int64, ctypes.c_int64, ctypes.c_int32, ctypes.c_void_p,
+                                           ctypes.c_void_p, ctypes.c_int32, ctypes.c_int] + [ctypes.c_void_p] * 4
+    assert sc(None, None, None, 1, 10, 2, None, None, 0, 0, p, p, p, None) == -1
+    assert sc(p, None, None, 1, 10, 2000, None, None, 0, 0, p, p, p, None) == -2
+    assert sc(p, None, None, 1, 10, 2, None, None, -1, 0, p, p, p, None) == -1
+    al = lib.hdl_allocate_continuations
+    al.restype = ctypes.c_int
+    al.argtypes = [ctypes.c_void_p, ctypes.c_void_p, ctypes.c_int64, ctypes.c_int32, ctypes.c_void_p,
+                   ctypes.c_int32, ctypes.c_void_p, ctypes.c_void_p, ctypes.c_void_p]
+    neg = (ctypes.c_int32 * 2)(3, -1)
+    zero = (ctypes.c_int32 * 2)(0, 0)
+    assert al(p, p, 4, 2, ctypes.addressof(neg), 0, p, None, None) == -1
+    assert al(p, p, 4, 2, ctypes.addressof(zero), 0, p, None, None) == -1
+    assert al(p, p, 4, 17, ctypes.addressof(zero), 0, p, None, None) == -2
+    ga = lib.hdl_group_advantages
+    ga.restype = ctypes.c_int
+    ga.argtypes = [ctypes.c_void_p, ctypes.c_int64, ctypes.c_int32, ctypes.c_void_p, ctypes.c_void_p]
+    assert ga(p, 0, 16, p, None) == -1 and ga(None, 4, 16, p, None) == -1
+    pg = lib.hdl_policy_loss_grad
+    pg.restype = ctypes.c_int
+    pg.argtypes = [ctypes.c_void_p, ctypes.c_int64] + [ctypes.c_void_p] * 6 + [ctypes.c_int64, ctypes.c_float,
+                                                                                ctypes.c_float, ctypes.c_float,
+                                                                                ctypes.c_void_p, ctypes.c_void_p,
+                                                                                ctypes.c_void_p]
+    assert pg(p, 4, p, p, None, p, p, None, 10, 0.2, 0.28, 1.0, p, None, None) == -1   # pos without start
+    assert pg(p, 4, p, None, None, p, p, None, 10, -0.2, 0.28, 1.0, p, None, None) == -1

@@ -495,3 +495,123 @@ def test_backward_closed_forms_and_invariants():
     z = H[0] @ W.T
     p = np.exp(z - z.max()); p /= p.sum()
     assert np.allclose(dHb[0], -g[0] * (p @ W), atol=1e-13)
+
+
+# ------------------------------------------------------- group construction
+def _greedy_by_repeated_argmax(sc, cand, k, min_gap):
+    # independent formulation of the refill rule: each step takes the best
+    # remaining candidate compatible with everything taken so far
+    kept = []
+    while len(kept) < k:
+        ok = [t for t in cand if t not in kept and all(abs(t - u) >= min_gap for u in kept)]
+        if not ok:
+            break
+        kept.append(max(ok, key=lambda t: (sc[t], -t)))
+    return kept
+
+
+def test_constrained_selection_fixture():
+    T = 60
+    s = np.zeros((1, T))
+    for t, v in ((10, 0.9), (12, 0.8), (30, 0.7), (50, 0.6), (33, 0.65)):
+        s[0, t] = v
+    z = np.zeros_like(s)
+    # drop mode: 12 is too close to 10 and is not replaced
+    idx, sc, cnt = O.select_constrained(z, s, None, 2, min_gap=5)
+    assert cnt.tolist() == [1] and idx[0].tolist() == [10, -1] and sc[0, 0] == 0.9
+    # refill: the walk continues to 30
+    idx, _, cnt = O.select_constrained(z, s, None, 2, min_gap=5, refill=True)
+    assert cnt.tolist() == [2] and idx[0].tolist() == [10, 30]
+    # index range [11, 40] removes 10 and 50; 33 is within 5 of 30; the third
+    # point is the lowest zero-score position at least 5 from 12 and 30
+    idx, _, cnt = O.select_constrained(z, s, None, 3, lo=[11], hi=[40], min_gap=5, refill=True)
+    assert idx[0].tolist() == [12, 30, 17] and cnt.tolist() == [3]
+    # value mode ranks the values themselves
+    idx, _, _ = O.select_constrained(s, None, None, 2)
+    assert idx[0].tolist() == [10, 12]
+
+
+def test_constrained_selection_reduces_and_matches_repeated_argmax():
+    lo_, hi_, mask = workloads.make_logp_pair(5, 200, seed=41, nan_rows=1)
+    a = O.select_constrained(lo_, hi_, mask, 7)
+    b = O.select_branch_points(lo_, hi_, mask, 7)
+    for x, y in zip(a, b):
+        assert np.array_equal(x, y)
+    _, s, elig = O.divergence(lo_, hi_, mask)
+    rng = np.random.default_rng(42)
+    for trial in range(30):
+        k = int(rng.integers(1, 6))
+        gap = int(rng.integers(2, 40))
+        L = rng.integers(0, 100, 5)
+        H = L + rng.integers(0, 120, 5)
+        idx, _, cnt = O.select_constrained(lo_, hi_, mask, k, lo=L, hi=H, min_gap=gap, refill=True)
+        for r in range(5):
+            cand = [t for t in range(200) if elig[r, t] and L[r] <= t <= H[r]]
+            want = _greedy_by_repeated_argmax(s[r], cand, k, gap)
+            assert idx[r, :cnt[r]].tolist() == want
+        # drop mode keeps a subset of the unconstrained top k, in rank order
+        idx_d, _, cnt_d = O.select_constrained(lo_, hi_, mask, k, lo=L, hi=H, min_gap=gap)
+        top, _, _ = O.select_constrained(lo_, hi_, mask, k, lo=L, hi=H)
+        for r in range(5):
+            kept = idx_d[r, :cnt_d[r]].tolist()
+            order = [t for t in top[r].tolist() if t in kept]
+            assert kept == order
+            for t in top[r].tolist():
+                if t >= 0 and t not in kept:
+                    assert any(abs(t - u) < gap for u in kept)
+
+
+def test_allocation_fixtures():
+    idx = np.array([[17, 40], [5, -1], [-1, -1]], np.int32)
+    pos, rank = O.allocate_continuations(idx, np.array([2, 1, 0]), (3, 4), fallback=0)
+    assert pos[0].tolist() == [17] * 3 + [40] * 4 and rank[0].tolist() == [0] * 3 + [1] * 4
+    assert pos[1].tolist() == [5] * 7 and rank[1].tolist() == [0] * 7
+    assert pos[2].tolist() == [0] * 7 and rank[2].tolist() == [-1] * 7
+    # 2 x 1 configuration (Table 5): all seven at the single point
+    pos, _ = O.allocate_continuations(np.array([[9]], np.int32), np.array([1]), (7,))
+    assert pos[0].tolist() == [9] * 7
+
+
+def test_group_advantages_closed_forms():
+    R = np.array([[1.0, 0.0, 0.0, 1.0], [0.3, 0.3, 0.3, 0.3]])
+    A = O.group_advantages(R)
+    assert np.allclose(A[0], [0.5, -0.5, -0.5, 0.5]) and np.all(A[1] == 0)
+    rng = np.random.default_rng(3)
+    X = rng.normal(size=(5, 16))
+    assert np.allclose(O.group_advantages(X).sum(axis=1), 0.0, atol=1e-14)
+    assert np.allclose(O.group_advantages(X + 7.0), O.group_advantages(X), atol=1e-13)
+
+
+def test_policy_loss_grad_by_finite_differences_and_clip_regions():
+    rng = np.random.default_rng(8)
+    n = 400
+    adv = rng.normal(size=6)
+    traj = rng.integers(0, 6, n)
+    lo_ = rng.normal(size=n) * 0.1 - 2
+    ln = lo_ + rng.normal(size=n) * 0.4
+    g, l = O.policy_loss_grad(adv, traj, ln, lo_, scale=0.01)
+    h = 1e-7
+    for i in range(n):
+        r = math.exp(ln[i] - lo_[i])
+        if min(abs(r - 0.8), abs(r - 1.28)) < 1e-3:
+            continue   # not differentiable at the clip boundaries
+        lp = ln.copy(); lp[i] += h
+        lm = ln.copy(); lm[i] -= h
+        num = (O.policy_loss_grad(adv, traj[i:i+1], lp[i:i+1], lo_[i:i+1], scale=0.01)[1][0] -
+               O.policy_loss_grad(adv, traj[i:i+1], lm[i:i+1], lo_[i:i+1], scale=0.01)[1][0]) / (2 * h)
+        assert abs(num - g[i]) <= 1e-6 * max(1.0, abs(g[i]))
+        # the clipped side carries no gradient
+        if adv[traj[i]] > 0 and r > 1.28:
+            assert g[i] == 0.0
+        if adv[traj[i]] < 0 and r < 0.8:
+            assert g[i] == 0.0
+    # on-policy (r = 1): g = -scale * A
+    g1, _ = O.policy_loss_grad(adv, traj, lo_, lo_, scale=0.5)
+    assert np.allclose(g1, -0.5 * adv[traj])
+    # a continuation's reused prefix and masked tokens carry nothing
+    pos = np.arange(n) % 50
+    start = np.array([0, 10, 0, 30, 0, 0])
+    mask = (rng.random(n) < 0.8).astype(np.uint8)
+    g2, _ = O.policy_loss_grad(adv, traj, ln, lo_, mask, pos, start)
+    off = (mask == 0) | (pos < start[traj])
+    assert np.all(g2[off] == 0.0)
