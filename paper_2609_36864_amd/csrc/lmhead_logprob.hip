@@ -330,9 +330,11 @@ __global__ __launch_bounds__(kThreads, 1) void lmhead_logprob_kernel(LmheadArgs 
   };
 
   // Gradient mode: G = g (1[v == y] - p) for the 4 x kNB blocks of this wave,
-  // rounded to bf16 and stored as 4 consecutive vocabulary entries (8 bytes)
-  // per accumulator run.  Rows >= V hold -inf, so p = 0 and G = 0 there,
-  // which zero-fills the columns up to g_cols.
+  // rounded to bf16.  A lane holds 4-row runs 8 rows apart; lanes l and
+  // l + 32 exchange half of their runs so that each ends with 16 consecutive
+  // vocabulary entries of its token row (32 bytes, two 16-byte stores).
+  // Rows >= V hold -inf, so p = 0 and G = 0 there, which zero-fills the
+  // columns up to g_cols.
   auto grad_epilogue = [&](int64_t vt) {
     const int64_t vbase = vt * kTileV + wm * 128;
 #pragma unroll
@@ -340,25 +342,39 @@ __global__ __launch_bounds__(kThreads, 1) void lmhead_logprob_kernel(LmheadArgs 
       const int64_t e = rt * kTileN + wn * kWaveN + bn * 32 + col;
       uint16_t* grow = p.g_out + e * p.g_ld;
 #pragma unroll
-      for (int bm = 0; bm < 4; ++bm)
+      for (int bm = 0; bm < 4; ++bm) {
+        uint32_t pk[4][2];   // [run jr][pair]: rows 8 jr + 4 half + {0,1 | 2,3}
 #pragma unroll
-        for (int jr = 0; jr < 4; ++jr) {
-          const int64_t v0 = vbase + bm * 32 + 8 * jr + 4 * half;
-          uint32_t packed[2];
+        for (int jr = 0; jr < 4; ++jr)
 #pragma unroll
           for (int r = 0; r < 4; r += 2) {
+            const int64_t v = vbase + bm * 32 + 8 * jr + 4 * half + r;
             float gv[2];
 #pragma unroll
             for (int u = 0; u < 2; ++u) {
               const float pv = fast_exp2(__builtin_fmaf(acc[bm][bn][jr * 4 + r + u], kLog2e, -g_lse[bn]));
-              gv[u] = (v0 + r + u == tok[bn]) ? g_up[bn] * (1.f - pv) : -g_up[bn] * pv;
+              gv[u] = (v + u == tok[bn]) ? g_up[bn] * (1.f - pv) : -g_up[bn] * pv;
             }
-            packed[r / 2] = static_cast<uint32_t>(__builtin_bit_cast(uint16_t, static_cast<__bf16>(gv[0]))) |
+            pk[jr][r / 2] = static_cast<uint32_t>(__builtin_bit_cast(uint16_t, static_cast<__bf16>(gv[0]))) |
                             (static_cast<uint32_t>(__builtin_bit_cast(uint16_t, static_cast<__bf16>(gv[1]))) << 16);
           }
-          if (e < n_s && v0 < p.g_cols)
-            *reinterpret_cast<uint2*>(grow + v0) = make_uint2(packed[0], packed[1]);
+        // lane half 0 keeps runs 0, 1 and takes its partner's; half 1 keeps 2, 3
+        uint32_t rv[4];
+#pragma unroll
+        for (int q = 0; q < 4; ++q) {
+          const uint32_t send = half == 0 ? pk[2 + q / 2][q % 2] : pk[q / 2][q % 2];
+          rv[q] = static_cast<uint32_t>(__shfl_xor(static_cast<int>(send), 32));
         }
+        const uint4 lo = half == 0 ? make_uint4(pk[0][0], pk[0][1], rv[0], rv[1])
+                                   : make_uint4(rv[0], rv[1], pk[2][0], pk[2][1]);
+        const uint4 hi = half == 0 ? make_uint4(pk[1][0], pk[1][1], rv[2], rv[3])
+                                   : make_uint4(rv[2], rv[3], pk[3][0], pk[3][1]);
+        const int64_t v16 = vbase + bm * 32 + 16 * half;   // first of this lane's 16 entries
+        if (e < n_s && v16 < p.g_cols) {
+          *reinterpret_cast<uint4*>(grow + v16) = lo;
+          *reinterpret_cast<uint4*>(grow + v16 + 8) = hi;
+        }
+      }
     }
 #pragma unroll
     for (int bm = 0; bm < 4; ++bm)
@@ -367,6 +383,7 @@ __global__ __launch_bounds__(kThreads, 1) void lmhead_logprob_kernel(LmheadArgs 
 #pragma unroll
         for (int q = 0; q < 16; ++q) acc[bm][bn][q] = 0.f;
   };
+
 
   // ---- pipelined main loop over (V-tile, K-slice) ------------------------
   const int n_pre = n_iter < kStages ? n_iter : kStages;
