@@ -278,3 +278,31 @@ def test_boundary_errors(hdl):
     with pytest.raises(hdl.HdlError) as e:
         hdl.token_logprobs(H, W, y, workspace=small)
     assert e.value.status == -3
+
+
+def test_hidden_states_over_4gib_split_into_launches(hdl):
+    # 525,065 rows of d = 4096 bf16 (4.3 GB): the library cuts the call into
+    # launches of 2^32 / 8192 = 524,288 rows (32-bit DMA offsets); rows on
+    # both sides of the cut must match the oracle and masked rows stay 0
+    n, d, V = 524288 + 777, 4096, 1000
+    gen = torch.Generator(device="cuda").manual_seed(77)
+    H = torch.randn(n, d, device="cuda", generator=gen).to(torch.bfloat16)
+    W = (torch.randn(V, d, device="cuda", generator=gen) * 0.02).to(torch.bfloat16)
+    y = torch.randint(0, V, (n,), device="cuda", dtype=torch.int32, generator=gen)
+    m = (torch.rand(n, device="cuda", generator=gen) < 0.9).to(torch.uint8)
+    lp, lse = hdl.token_logprobs(H, W, y, m)
+    torch.cuda.synchronize()
+    rows = np.array([0, 1, 1000, 524286, 524287, 524288, 524289, 524290, 524800, n - 1])
+    mk = m[torch.as_tensor(rows, device="cuda")].cpu().numpy()
+    Hs = H[torch.as_tensor(rows, device="cuda")].cpu()
+    want, want_lse = O.token_logprobs(as_f64(Hs), as_f64(W.cpu()), y[torch.as_tensor(rows, device="cuda")].cpu().numpy())
+    got = lp[torch.as_tensor(rows, device="cuda")].cpu().numpy()
+    on = mk != 0
+    assert np.abs(got[on] - want[on]).max() <= TOL_BF16
+    assert np.all(got[~on] == 0.0)
+    del H
+    torch.cuda.empty_cache()
+    # the backward pass keeps one launch and refuses this size
+    with pytest.raises(ValueError):
+        hdl.token_logprobs_backward(torch.zeros(n, d, dtype=torch.bfloat16, device="cuda"), W, y, m, lse,
+                                    torch.zeros(n, device="cuda"))
