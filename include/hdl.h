@@ -213,7 +213,7 @@ int hdl_token_logprobs_backward(const void* hidden, const void* w_vocab, const i
  *            (0 or 1: no spacing constraint).
  *  refill    0: rank the k best candidates and drop, in rank order, any point
  *            closer than min_gap to a better retained one (a root may end with
- *            fewer than k points -- the paper's "only one is retained");
+ *            fewer than k points, as in the paper when two points are too close);
  *            1: walk down the ranking (at most the best HDL_MAX_K candidates)
  *            until k points are retained.
  *  idx, score [n_roots, k], count [n_roots]: retained points in rank order
