@@ -254,6 +254,27 @@ def main() -> int:
                      "kernel": "lmhead_logprob_kernel", "kernel_ms": kern_avg_ms,
                      "flops_per_launch": flops},
     }
+    if not ent_sel:
+        # the divergence / top-k pass alone (a6-a7): HBM-bound in principle,
+        # latency-bound at these sizes (one workgroup per root)
+        lp = logp.view(2, c.R, c.T)
+        hdl.select_branch_points(lp[0], lp[1], mask_rt, c.k)
+        stream = torch.cuda.current_stream(dev)
+        e2 = torch.cuda.Event(enable_timing=True)
+        e3 = torch.cuda.Event(enable_timing=True)
+        reps = 50
+        torch.cuda.synchronize()
+        e2.record(stream)
+        for _ in range(reps):
+            hdl.select_branch_points(lp[0], lp[1], mask_rt, c.k)
+        e3.record(stream)
+        torch.cuda.synchronize()
+        sel_ms = e2.elapsed_time(e3) / reps
+        sel_bytes = c.R * c.T * (4 + 4 + 1) + c.R * c.k * 8 + c.R * 4
+        result["select_pass"] = {"kernel": "select_kernel", "bound": "latency (one workgroup per root)",
+                                 "ms_per_call": sel_ms, "bytes_per_call": sel_bytes,
+                                 "achieved_GBps": sel_bytes / (sel_ms * 1e-3) / 1e9, "peak_GBps": 8000.0}
+        log(f"divergence/top-k pass: {sel_ms * 1e3:.1f} us per call, {sel_bytes} bytes")
     if args.copy_probe_mb > 0:
         src = torch.empty(args.copy_probe_mb << 20, dtype=torch.uint8, device=dev).fill_(1)
         dst = torch.empty_like(src)
