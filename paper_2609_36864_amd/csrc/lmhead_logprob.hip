@@ -15,7 +15,7 @@
 // the V-tiles of one chunk.  Eight waves per workgroup (two per SIMD, so one
 // wave's memory and epilogue work overlaps the other's MFMAs), each owning
 // 128 vocab x 64 tokens as a 4x2 grid of 32x32 MFMA blocks with fp32
-// accumulators (HDL_WAVES=4 selects one wave per SIMD with 128 x 128 each).
+// accumulators.
 // W is the MFMA "A" operand (vocabulary on the M axis) and the hidden states
 // are the "B" operand (tokens on the N axis), so each lane's accumulators
 // hold one token column and 64 vocabulary rows: the online max / sum-of-exp
@@ -23,8 +23,7 @@
 // only once per work item.
 //
 // Operands stream through LDS in K-slices of 128 bytes per row (64 bf16 or
-// 32 fp32; HDL_LDS_CHUNKS=4 selects 64-byte slices) through a ring of
-// HDL_LDS_STAGES stages (default 2, 128 KB): the next slice is in flight
+// 32 fp32) through a ring of 2 stages (128 KB): the next slice is in flight
 // (global -> LDS DMA, no VGPR staging) while slice i is multiplied.  16-byte
 // chunks are XOR swizzled so that the 32-row fragment reads are bank-conflict
 // free.  The DMA is issued from inline assembly (wave-uniform 64-bit base +

@@ -13,21 +13,12 @@ namespace tile {
 typedef __bf16 bf16x8_t __attribute__((ext_vector_type(8)));
 typedef float f32x16_t __attribute__((ext_vector_type(16)));
 
-#ifndef HDL_WAVES
-#define HDL_WAVES 8
-#endif
-constexpr int kWaves = HDL_WAVES;                   // 4: one wave per SIMD; 8: two
+constexpr int kWaves = 8;                           // two waves per SIMD
 constexpr int kThreads = 64 * kWaves;
-constexpr int kNB = kWaves == 4 ? 4 : 2;            // 32-token MFMA blocks per wave
-constexpr int kWaveN = 32 * kNB;                    // tokens per wave (128 or 64)
-#ifndef HDL_LDS_CHUNKS
-#define HDL_LDS_CHUNKS 8
-#endif
-#ifndef HDL_LDS_STAGES
-#define HDL_LDS_STAGES 2
-#endif
-constexpr int kChunks = HDL_LDS_CHUNKS;             // 16-byte chunks per LDS row per stage
-constexpr int kStages = HDL_LDS_STAGES;             // LDS ring depth (K-slices)
+constexpr int kNB = 2;                              // 32-token MFMA blocks per wave
+constexpr int kWaveN = 32 * kNB;                    // tokens per wave
+constexpr int kChunks = 8;                          // 16-byte chunks per LDS row per stage (128-byte K-slices)
+constexpr int kStages = 2;                          // LDS ring depth (K-slices)
 constexpr int kSlots = kTileV * kChunks;            // uint4 slots per operand per stage
 constexpr int kBlockRows = 64 / kChunks;            // rows per 1 KB DMA block
 constexpr int kBlocksPerWave = kTileV / kBlockRows / kWaves;   // DMA blocks per operand per wave
@@ -37,29 +28,15 @@ constexpr float kLog2e = 1.4426950408889634f;
 constexpr float kNegInf = -__builtin_inff();
 
 static_assert(kTileV == kTileN, "square workgroup tile assumed");
-static_assert(kWaves == 4 || kWaves == 8, "4 or 8 waves");
-static_assert(kChunks == 4 || kChunks == 8, "64- or 128-byte K-slices");
 static_assert(kStages * 2 * kSlots * 16 <= 160 * 1024, "LDS ring exceeds 160 KB");
 static_assert(kDmaPerSlice * (kStages - 1) <= 63, "vmcnt range");
 
-#ifndef HDL_SWZ
-#define HDL_SWZ 1
-#endif
 // XOR pattern of a row: the rows of one 32-row fragment read must land in
 // distinct 16-byte bank groups whether the LDS serves 8 or 16 lanes of a
 // ds_read_b128 per cycle.  With 128-byte rows, (row & 7) ^ ((row >> 3) & 1)
 // does both: 8 consecutive rows get 8 distinct chunks, and rows r and r+8
 // (same bank half when two rows share a 256-byte bank line) differ too.
-__device__ __forceinline__ int row_xor(int row) {
-  if (kChunks == 8) {
-    if (HDL_SWZ == 0) return row & 7;
-    if (HDL_SWZ == 1) return (row & 7) ^ ((row >> 3) & 1);
-    return (row >> 1) & 7;
-  }
-  if (HDL_SWZ == 0) return (row >> 1) & 3;
-  if (HDL_SWZ == 1) return ((row >> 1) & 3) ^ ((row >> 3) & 1);
-  return (row >> 2) & 3;
-}
+__device__ __forceinline__ int row_xor(int row) { return (row & 7) ^ ((row >> 3) & 1); }
 
 // Slot of (row, logical 16-byte chunk) in a [rows][kChunks] LDS tile.
 __device__ __forceinline__ int swz(int row, int chunk) {
@@ -86,15 +63,15 @@ __device__ __forceinline__ void dma16(uint64_t sbase, uint32_t voff, uint32_t ld
       : "memory");
 }
 
-// Wait until at most `slices` K-slices of this lane's DMA are outstanding.
+// Wait until at most N of this lane's memory loads (DMAs) are outstanding.
 template <int N>
 __device__ __forceinline__ void wait_vmcnt() {
   asm volatile("s_waitcnt vmcnt(%0)" ::"n"(N) : "memory");
 }
+// Wait until at most `slices` K-slices (0 or 1 with a 2-stage ring) of this
+// lane's DMA are outstanding.
 __device__ __forceinline__ void wait_dma(int slices) {
-  if (kStages > 3 && slices >= 3) wait_vmcnt<(kStages > 3 ? 3 : 0) * kDmaPerSlice>();
-  else if (kStages > 2 && slices >= 2) wait_vmcnt<(kStages > 2 ? 2 : 0) * kDmaPerSlice>();
-  else if (slices >= 1) wait_vmcnt<kDmaPerSlice>();
+  if (slices >= 1) wait_vmcnt<kDmaPerSlice>();
   else wait_vmcnt<0>();
 }
 
