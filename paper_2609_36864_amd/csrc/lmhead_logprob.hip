@@ -9,7 +9,11 @@
 //
 // without ever storing z.  The vocabulary is cut into chunks; each work item
 // (row tile x chunk) leaves a partial (max, sum of exp, captured z_y) per row,
-// and merge_kernel combines the chunk partials in a fixed order.
+// and merge_kernel combines the chunk partials in a fixed order.  Two more
+// epilogues share the same main loop: one also accumulates the next-token
+// entropy (the Entropy localization baseline), the other writes the gradient
+// of log p with respect to the logits for the backward pass (the logits are
+// recomputed there, given the forward pass's log-sum-exp).
 //
 // Work item: 256 vocabulary rows x 256 token rows per V-tile, looping over
 // the V-tiles of one chunk.  Eight waves per workgroup (two per SIMD, so one
@@ -45,7 +49,6 @@ namespace {
 
 using namespace tile;
 
-
 // t of a state, moved from its own max m to a larger max mn:
 //   sum exp(z - mn) * (z - mn) log2(e) = f * (t + (m - mn) log2(e) * s),  f = exp(m - mn).
 // An empty state (m = -inf, s = t = 0) stays 0.
@@ -72,7 +75,6 @@ __device__ __forceinline__ void combine(float& m, float& s, float& z, float& t, 
   m = mn;
   z = fmaxf(z, z2);
 }
-
 
 // KTAIL: d is not a multiple of the K-slice, so the last slice of every
 // row needs zero-filling (a separate instantiation keeps that work out of the
