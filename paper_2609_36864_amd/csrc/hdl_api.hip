@@ -390,6 +390,7 @@ int hdl_token_logprobs_backward(const void* hidden, const void* w_vocab, const i
                                 float* grad_w, int accumulate_w, void* workspace, size_t workspace_bytes,
                                 void* stream) {
   const char* fn = "hdl_token_logprobs_backward";
+  g_last_error[0] = '\0';
   if (!hidden || !w_vocab || !tokens || !lse || !grad_logp || !grad_hidden || !grad_w)
     return fail(HDL_ERR_INVALID_ARG, "%s: null required pointer", fn);
   if (n_rows <= 0 || d <= 0 || vocab <= 0)
