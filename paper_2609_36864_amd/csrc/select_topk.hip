@@ -31,6 +31,10 @@ namespace {
 
 constexpr int kThreads = 1024;
 constexpr int kWaves = kThreads / 64;
+// Roots with at most this many positions keep their candidate keys in LDS
+// after the first pass (128 KB), so the radix passes and the collect scan
+// do not re-read global memory; longer roots recompute them each pass.
+constexpr int kStageMax = 32768;
 
 struct Scratch {
   int wsum[kWaves];
@@ -39,6 +43,7 @@ struct Scratch {
   int rank;
   unsigned long long keys[kThreads];
   int kept;
+  unsigned staged[kStageMax];   // candidate key per position, 0 = not a candidate
 };
 
 __device__ __forceinline__ int wave_incl_scan(int v) {
@@ -107,6 +112,18 @@ __device__ __forceinline__ Pos load_cand(bool values, const float* lo, const flo
   return p;
 }
 
+// Candidate key of position t: from LDS when the root is staged, else
+// recomputed from global memory (0: not a candidate; every candidate's key
+// is at least 0x00800000, the key of the most negative finite float).
+template <bool VALUES>
+__device__ __forceinline__ unsigned cand_key(const Scratch& sh, bool staged, const float* lo, const float* lh,
+                                             const uint8_t* mask, int64_t base, int64_t t, int64_t t_lo,
+                                             int64_t t_hi) {
+  if (staged) return sh.staged[t];
+  const Pos p = load_cand(VALUES, lo, lh, mask, base, t, t_lo, t_hi);
+  return p.elig ? p.key : 0u;
+}
+
 // pool: winners ranked before the spacing filter (k without refill);
 // min_gap <= 1 disables the filter; r_lo / r_hi (optional) bound the range.
 template <bool VALUES>
@@ -129,11 +146,14 @@ __global__ __launch_bounds__(kThreads) void select_kernel(const float* __restric
   const int64_t t_hi = r_hi ? r_hi[r] : T - 1;
 
   // ---- eligibility count (and the optional signed delta) -----------------
+  const bool staged = T <= kStageMax;
   int c = 0;
   for (int64_t t = tid; t < T; t += kThreads) {
     const Pos p = load_pos<VALUES>(lo, lh, mask, base, t);
     if (delta_out) delta_out[base + t] = p.delta;
-    c += (p.elig && t >= t_lo && t <= t_hi) ? 1 : 0;
+    const bool cand = p.elig && t >= t_lo && t <= t_hi;
+    if (staged) sh.staged[t] = cand ? p.key : 0u;
+    c += cand ? 1 : 0;
   }
   int n_elig;
   block_excl_scan(c, &n_elig, sh);
@@ -147,8 +167,8 @@ __global__ __launch_bounds__(kThreads) void select_kernel(const float* __restric
       for (int i = tid; i < 256; i += kThreads) sh.hist[i] = 0;
       __syncthreads();
       for (int64_t t = tid; t < T; t += kThreads) {
-        const Pos p = load_cand(VALUES, lo, lh, mask, base, t, t_lo, t_hi);
-        if (p.elig && (p.key & pmask) == prefix) atomicAdd(&sh.hist[(p.key >> shift) & 255], 1);
+        const unsigned key = cand_key<VALUES>(sh, staged, lo, lh, mask, base, t, t_lo, t_hi);
+        if (key != 0u && (key & pmask) == prefix) atomicAdd(&sh.hist[(key >> shift) & 255], 1);
       }
       __syncthreads();
       // Inclusive scan over bins from the top digit down; the bin in which
@@ -174,8 +194,8 @@ __global__ __launch_bounds__(kThreads) void select_kernel(const float* __restric
     for (int64_t t0 = 0; t0 < T; t0 += kThreads) {
       const int64_t t = t0 + tid;
       Pos p;
-      if (t < T) p = load_cand(VALUES, lo, lh, mask, base, t, t_lo, t_hi);
-      else { p.elig = false; p.key = 0; p.delta = 0.f; }
+      p.key = t < T ? cand_key<VALUES>(sh, staged, lo, lh, mask, base, t, t_lo, t_hi) : 0u;
+      p.elig = p.key != 0u;
       const bool eq = p.elig && p.key == thr;
       int n_eq;
       const int tie_rank = ties_before + block_excl_scan(eq ? 1 : 0, &n_eq, sh);
