@@ -90,6 +90,8 @@ def load_library() -> ctypes.CDLL:
     L.hdl_profile_enable.restype = ctypes.c_int
     L.hdl_profile_read.argtypes = [ctypes.POINTER(ctypes.c_double), ctypes.POINTER(c_i64)]
     L.hdl_profile_read.restype = ctypes.c_int
+    L.hdl_profile_read_kind.argtypes = [ctypes.c_int, ctypes.POINTER(ctypes.c_double), ctypes.POINTER(c_i64)]
+    L.hdl_profile_read_kind.restype = ctypes.c_int
     _LIB = L
     return L
 
@@ -425,9 +427,13 @@ def profile_enable(on: bool = True) -> None:
     _check(load_library().hdl_profile_enable(1 if on else 0))
 
 
-def profile_read() -> Tuple[float, int]:
-    """(summed fused-kernel milliseconds, launches) since the last read."""
+PROFILE_LMHEAD, PROFILE_GRAD, PROFILE_GEMM = 0, 1, 2
+
+
+def profile_read(kind: int = PROFILE_LMHEAD) -> Tuple[float, int]:
+    """(summed milliseconds, launches) of one kernel kind since its last read:
+    the fused lm-head kernel (default), its gradient mode, or the backward GEMMs."""
     ms = ctypes.c_double(0.0)
     n = ctypes.c_int64(0)
-    _check(load_library().hdl_profile_read(ctypes.byref(ms), ctypes.byref(n)))
+    _check(load_library().hdl_profile_read_kind(int(kind), ctypes.byref(ms), ctypes.byref(n)))
     return float(ms.value), int(n.value)

@@ -34,13 +34,48 @@ bool aligned(const void* p, size_t a) { return (reinterpret_cast<uintptr_t>(p) %
 size_t round_up(size_t x, size_t a) { return (x + a - 1) / a * a; }
 
 // ---- kernel timing (measurement tools only) ------------------------------
+// Kinds: HDL_PROFILE_LMHEAD (fused lm-head kernel, statistics or entropy),
+// HDL_PROFILE_GRAD (its gradient mode), HDL_PROFILE_GEMM (backward GEMMs).
+constexpr int kProfileKinds = 3;
+using EventPair = std::pair<hipEvent_t, hipEvent_t>;
 struct Profiler {
   std::mutex mu;
   bool on = false;
-  std::vector<std::pair<hipEvent_t, hipEvent_t>> pending;
-  std::vector<std::pair<hipEvent_t, hipEvent_t>> spare;
+  std::vector<EventPair> pending[kProfileKinds];
+  std::vector<EventPair> spare;
 };
 Profiler g_prof;
+
+// A timed launch: start() records the first event on the stream if timing
+// is on, stop() the second one and files the pair under its kind.
+struct TimedLaunch {
+  EventPair ev{nullptr, nullptr};
+  bool timed = false;
+  hipError_t start(hipStream_t s) {
+    {
+      std::lock_guard<std::mutex> lk(g_prof.mu);
+      if (!g_prof.on) return hipSuccess;
+      if (!g_prof.spare.empty()) {
+        ev = g_prof.spare.back();
+        g_prof.spare.pop_back();
+      } else {
+        hipError_t e = hipEventCreate(&ev.first);
+        if (e == hipSuccess) e = hipEventCreate(&ev.second);
+        if (e != hipSuccess) return e;
+      }
+      timed = true;
+    }
+    return hipEventRecord(ev.first, s);
+  }
+  hipError_t stop(int kind, hipStream_t s) {
+    if (!timed) return hipSuccess;
+    hipError_t e = hipEventRecord(ev.second, s);
+    if (e != hipSuccess) return e;
+    std::lock_guard<std::mutex> lk(g_prof.mu);
+    g_prof.pending[kind].push_back(ev);
+    return hipSuccess;
+  }
+};
 
 }  // namespace
 
@@ -170,28 +205,11 @@ int token_stats(const char* fn, const void* hidden, const void* w_vocab, const i
     a.row_base = 0;
     a.row_cap = n;
 
-    std::pair<hipEvent_t, hipEvent_t> ev{nullptr, nullptr};
-    bool timed = false;
-    {
-      std::lock_guard<std::mutex> lk(g_prof.mu);
-      if (g_prof.on) {
-        if (!g_prof.spare.empty()) {
-          ev = g_prof.spare.back();
-          g_prof.spare.pop_back();
-        } else if (hipEventCreate(&ev.first) != hipSuccess || hipEventCreate(&ev.second) != hipSuccess) {
-          return fail(HDL_ERR_HIP, "%s: hipEventCreate failed", fn);
-        }
-        timed = true;
-      }
-    }
-    if (timed && (e = hipEventRecord(ev.first, s)) != hipSuccess) return hip_fail(e, "hipEventRecord");
+    TimedLaunch tl;
+    if ((e = tl.start(s)) != hipSuccess) return hip_fail(e, "timing event");
     e = hdl::launch_lmhead(a, lp.grid, dtype == HDL_BF16, s);
     if (e != hipSuccess) return hip_fail(e, "lm-head kernel launch");
-    if (timed) {
-      if ((e = hipEventRecord(ev.second, s)) != hipSuccess) return hip_fail(e, "hipEventRecord");
-      std::lock_guard<std::mutex> lk(g_prof.mu);
-      g_prof.pending.push_back(ev);
-    }
+    if ((e = tl.stop(HDL_PROFILE_LMHEAD, s)) != hipSuccess) return hip_fail(e, "timing event");
     e = hdl::launch_merge(a, n, logp_c, lse_c, ent_c, s);
     if (e != hipSuccess) return hip_fail(e, "merge kernel launch");
   }
@@ -272,7 +290,7 @@ const char* hdl_status_string(int status) {
 
 const char* hdl_last_error(void) { return g_last_error; }
 
-int hdl_abi_version(void) { return 4; }
+int hdl_abi_version(void) { return 5; }
 
 int hdl_profile_enable(int on) {
   std::lock_guard<std::mutex> lk(g_prof.mu);
@@ -281,10 +299,15 @@ int hdl_profile_enable(int on) {
 }
 
 int hdl_profile_read(double* total_ms, int64_t* launches) {
+  return hdl_profile_read_kind(HDL_PROFILE_LMHEAD, total_ms, launches);
+}
+
+int hdl_profile_read_kind(int kind, double* total_ms, int64_t* launches) {
+  if (kind < 0 || kind >= kProfileKinds) return fail(HDL_ERR_INVALID_ARG, "hdl_profile_read_kind: kind %d", kind);
   std::lock_guard<std::mutex> lk(g_prof.mu);
   double tot = 0.0;
   int64_t n = 0;
-  for (auto& ev : g_prof.pending) {
+  for (auto& ev : g_prof.pending[kind]) {
     hipError_t e = hipEventSynchronize(ev.second);
     if (e != hipSuccess) return hip_fail(e, "hipEventSynchronize");
     float ms = 0.f;
@@ -294,7 +317,7 @@ int hdl_profile_read(double* total_ms, int64_t* launches) {
     ++n;
     g_prof.spare.push_back(ev);
   }
-  g_prof.pending.clear();
+  g_prof.pending[kind].clear();
   if (total_ms) *total_ms = tot;
   if (launches) *launches = n;
   return HDL_OK;
@@ -458,7 +481,10 @@ int hdl_token_logprobs_backward(const void* hidden, const void* w_vocab, const i
     a.g_out = g;
     a.g_ld = plan.v_pad;
     a.g_cols = plan.v_pad;
+    TimedLaunch tg_;
+    if ((e = tg_.start(s)) != hipSuccess) return hip_fail(e, "timing event");
     if ((e = hdl::launch_lmhead_grad(a, plan.fwd.grid, s)) != hipSuccess) return hip_fail(e, "gradient kernel launch");
+    if ((e = tg_.stop(HDL_PROFILE_GRAD, s)) != hipSuccess) return hip_fail(e, "timing event");
     // 2. G^T and the chunk's hidden rows transposed, zero beyond the scored rows
     hdl::TransposeArgs tg{};
     tg.in = g;
@@ -491,7 +517,10 @@ int hdl_token_logprobs_backward(const void* hidden, const void* w_vocab, const i
     gh.k_split = plan.k_split;
     gh.splits = plan.splits;
     gh.c_split_stride = plan.nc * d;
+    TimedLaunch th_;
+    if ((e = th_.start(s)) != hipSuccess) return hip_fail(e, "timing event");
     if ((e = hdl::launch_gemm_nt(gh, s)) != hipSuccess) return hip_fail(e, "GEMM launch");
+    if ((e = th_.stop(HDL_PROFILE_GEMM, s)) != hipSuccess) return hip_fail(e, "timing event");
     if ((e = hdl::launch_splitk_scatter(hpart, plan.splits, plan.nc * d, d, rows + base, n_scored, base, plan.nc,
                                         grad_hidden, s)) != hipSuccess)
       return hip_fail(e, "split-K sum launch");
@@ -501,7 +530,10 @@ int hdl_token_logprobs_backward(const void* hidden, const void* w_vocab, const i
     gw.dyn_base = base;
     gw.dyn_dim = 2;
     gw.beta = (c > 0 || accumulate_w) ? 1 : 0;
+    TimedLaunch tw_;
+    if ((e = tw_.start(s)) != hipSuccess) return hip_fail(e, "timing event");
     if ((e = hdl::launch_gemm_nt(gw, s)) != hipSuccess) return hip_fail(e, "GEMM launch");
+    if ((e = tw_.stop(HDL_PROFILE_GEMM, s)) != hipSuccess) return hip_fail(e, "timing event");
   }
   return HDL_OK;
 }

@@ -32,7 +32,7 @@ def test_header_declares_the_boundary():
               "hdl_select_top_k", "hdl_token_logprobs_workspace_size", "hdl_status_string",
               "hdl_last_error", "hdl_token_logprobs_backward", "hdl_token_logprobs_backward_workspace_size",
               "hdl_select_constrained", "hdl_allocate_continuations", "hdl_group_advantages",
-              "hdl_policy_loss_grad"):
+              "hdl_policy_loss_grad", "hdl_profile_enable", "hdl_profile_read", "hdl_profile_read_kind"):
         assert n in names
 
 
@@ -45,7 +45,7 @@ def test_status_strings(lib):
     assert lib.hdl_status_string(0) == b"ok"
     for s in (-1, -2, -3, -4):
         assert lib.hdl_status_string(s) not in (b"ok", b"unknown status")
-    assert lib.hdl_abi_version() == 4
+    assert lib.hdl_abi_version() == 5
 
 
 def test_workspace_size_rules(lib):
