@@ -75,7 +75,9 @@ size_t hdl_token_logprobs_workspace_size(int64_t n_rows, int64_t d, int64_t voca
  *                        16-byte aligned.
  *  tokens   [n_rows]     int32 sampled tokens.  Precondition: 0 <= t < vocab;
  *                        a row that violates it gets logp = NaN (never an
- *                        error).
+ *                        error).  A NaN or infinite hidden-state element
+ *                        likewise gives its row logp = NaN and lse = NaN; the
+ *                        other rows are unaffected.
  *  mask     [n_rows]     uint8, or NULL for "all rows".  Only rows with
  *                        mask != 0 (policy-generated tokens, Sec. 3.1) are
  *                        computed; the others get logp = 0 and lse = 0 and

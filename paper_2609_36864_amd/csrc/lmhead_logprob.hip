@@ -534,8 +534,9 @@ __global__ __launch_bounds__(256) void merge_kernel(LmheadArgs p, float* __restr
   const int y = p.tokens[row];
   float lp = z - lse;
   // The exact value is <= 0; rounding in the fp32 normaliser can leave a
-  // positive residue of a few ulps when one logit dominates.
-  lp = lp < 0.f ? lp : 0.f;
+  // positive residue of a few ulps when one logit dominates.  (Written so
+  // that a NaN -- a non-finite hidden state -- stays NaN.)
+  lp = lp > 0.f ? 0.f : lp;
   if (y < 0 || y >= p.vocab) lp = __builtin_nanf("");
   logp[row] = lp;
   if (lse_out) lse_out[row] = lse;
@@ -543,7 +544,7 @@ __global__ __launch_bounds__(256) void merge_kernel(LmheadArgs p, float* __restr
     // The exact value is >= 0; clamp the rounding residue of a near one-hot
     // distribution.
     const float h = __builtin_fmaf(-0.6931471805599453f, t / s, __builtin_amdgcn_logf(s) * 0.6931471805599453f);
-    entropy[row] = h > 0.f ? h : 0.f;
+    entropy[row] = h < 0.f ? 0.f : h;
   }
 }
 

@@ -306,3 +306,28 @@ def test_hidden_states_over_4gib_split_into_launches(hdl):
     with pytest.raises(ValueError):
         hdl.token_logprobs_backward(torch.zeros(n, d, dtype=torch.bfloat16, device="cuda"), W, y, m, lse,
                                     torch.zeros(n, device="cuda"))
+
+
+def test_non_finite_hidden_row_stays_local(hdl):
+    # a NaN or Inf in one row's hidden state makes that row's log p NaN (its
+    # logits are NaN); every other row of the same tile is unaffected, and
+    # the selection never picks the poisoned position
+    g = torch.Generator().manual_seed(15)
+    R, T, d, V = 1, 600, 64, 3000
+    W = (torch.randn(V, d, generator=g) * 0.05).to(torch.bfloat16)
+    H = torch.randn(2 * T, d, generator=g).to(torch.bfloat16)
+    y = torch.randint(0, V, (2 * T,), generator=g, dtype=torch.int32)
+    clean, _ = run_logprobs(hdl, H, W, y, None)
+    Hbad = H.clone()
+    Hbad[T + 17, 5] = float("nan")        # hindsight row of position 17
+    Hbad[T + 300, 0] = float("inf")       # hindsight row of position 300
+    lp, _ = run_logprobs(hdl, Hbad, W, y, None)
+    bad = [T + 17, T + 300]
+    assert np.all(np.isnan(lp[bad]))
+    good = np.setdiff1d(np.arange(2 * T), bad)
+    assert np.array_equal(lp[good].view(np.uint32), clean[good].view(np.uint32))
+    lpt = torch.from_numpy(lp).cuda()
+    idx, _, count, _ = hdl.select_branch_points(lpt[:T].view(1, T), lpt[T:].view(1, T), None, T)
+    torch.cuda.synchronize()
+    chosen = idx[0, : int(count[0])].tolist()
+    assert int(count[0]) == T - 2 and 17 not in chosen and 300 not in chosen

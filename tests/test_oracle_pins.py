@@ -615,3 +615,16 @@ def test_policy_loss_grad_by_finite_differences_and_clip_regions():
     g2, _ = O.policy_loss_grad(adv, traj, ln, lo_, mask, pos, start)
     off = (mask == 0) | (pos < start[traj])
     assert np.all(g2[off] == 0.0)
+
+
+def test_non_finite_hidden_row_gives_nan_for_that_row_only():
+    rng = np.random.default_rng(16)
+    W = rng.normal(size=(50, 6))
+    H = rng.normal(size=(4, 6))
+    y = rng.integers(0, 50, 4)
+    clean, _ = O.token_logprobs(H, W, y)
+    H[1, 2] = np.nan
+    H[3, 0] = np.inf
+    lp, lse = O.token_logprobs(H, W, y)
+    assert np.isnan(lp[1]) and np.isnan(lp[3]) and np.isnan(lse[1])
+    assert np.array_equal(lp[[0, 2]], clean[[0, 2]])
