@@ -331,3 +331,29 @@ def test_non_finite_hidden_row_stays_local(hdl):
     torch.cuda.synchronize()
     chosen = idx[0, : int(count[0])].tolist()
     assert int(count[0]) == T - 2 and 17 not in chosen and 300 not in chosen
+
+
+def test_degenerate_vocabularies_and_large_logits(hdl):
+    g = torch.Generator().manual_seed(16)
+    n, d = 300, 64
+    H = torch.randn(n, d, generator=g).to(torch.bfloat16)
+    # V = 1: every log p is exactly 0; V = 2: the log-sigmoid, against the oracle
+    for V in (1, 2):
+        W = (torch.randn(V, d, generator=g) * 0.05).to(torch.bfloat16)
+        y = torch.randint(0, V, (n,), generator=g, dtype=torch.int32)
+        lp, lse = run_logprobs(hdl, H, W, y, None)
+        want, want_lse = oracle_rows(H, W, y, np.arange(n))
+        assert np.abs(lp - want).max() <= TOL_BF16 and np.abs(lse - want_lse).max() <= TOL_BF16
+        if V == 1:
+            assert np.all(lp == 0.0)
+    # logits of a few hundred: the online max keeps exp in range and the
+    # stated bar still holds (fp32 spacing at 1000 is 6e-5)
+    V = 5000
+    W = (torch.randn(V, d, generator=g) * 30.0).to(torch.bfloat16)
+    y = torch.randint(0, V, (n,), generator=g, dtype=torch.int32)
+    lp, lse = run_logprobs(hdl, H, W, y, None)
+    want, want_lse = oracle_rows(H, W, y, np.arange(n))
+    assert np.abs(want_lse).max() > 200
+    assert np.all(np.isfinite(lp))
+    err = np.abs(lp - want).max()
+    assert err <= TOL_BF16, f"max |log p error| {err:.3g} at |lse| up to {np.abs(want_lse).max():.0f}"
