@@ -12,6 +12,7 @@ built library or a GPU the calls raise.
 from __future__ import annotations
 
 import ctypes
+import functools
 import os
 from typing import Optional, Tuple
 
@@ -118,6 +119,23 @@ def _require_cuda(name: str, t: torch.Tensor) -> None:
         raise ValueError(f"{name} must be contiguous")
 
 
+def _on_tensor_device(fn):
+    """Run an entry point with its tensors' GPU as the current device (the
+    library launches on the current device and the stream of that device);
+    every GPU tensor argument must live on the same device."""
+    @functools.wraps(fn)
+    def wrapper(*args, **kwargs):
+        devs = {a.device for a in list(args) + list(kwargs.values())
+                if isinstance(a, torch.Tensor) and a.device.type == "cuda"}
+        if len(devs) > 1:
+            raise ValueError(f"{fn.__name__}: tensors on several devices {sorted(map(str, devs))}")
+        if devs:
+            with torch.cuda.device(devs.pop()):
+                return fn(*args, **kwargs)
+        return fn(*args, **kwargs)
+    return wrapper
+
+
 def abi_version() -> int:
     return int(load_library().hdl_abi_version())
 
@@ -138,6 +156,7 @@ def _workspace(device: torch.device, nbytes: int) -> torch.Tensor:
     return ws
 
 
+@_on_tensor_device
 def token_logprobs(hidden: torch.Tensor, w_vocab: torch.Tensor, tokens: torch.Tensor,
                    mask: Optional[torch.Tensor] = None, *, logp: Optional[torch.Tensor] = None,
                    lse: Optional[torch.Tensor] = None, want_lse: bool = True,
@@ -192,6 +211,7 @@ def token_logprobs(hidden: torch.Tensor, w_vocab: torch.Tensor, tokens: torch.Te
     return logp, lse
 
 
+@_on_tensor_device
 def select_branch_points(logp_orig: torch.Tensor, logp_hind: torch.Tensor,
                          mask: Optional[torch.Tensor], k: int, *, want_delta: bool = False):
     """|Delta log p| (Eq. 2) and the per-root top-k branch points (Sec. 3.2).
@@ -225,6 +245,7 @@ def select_branch_points(logp_orig: torch.Tensor, logp_hind: torch.Tensor,
     return idx, score, count, delta
 
 
+@_on_tensor_device
 def select_top_k(values: torch.Tensor, mask: Optional[torch.Tensor], k: int):
     """Per-root top-k of a per-position value, e.g. next-token entropy for the
     Entropy localization baseline (Sec. 4.1).  values [R, T] fp32, mask
@@ -250,6 +271,7 @@ def select_top_k(values: torch.Tensor, mask: Optional[torch.Tensor], k: int):
     return idx, score, count
 
 
+@_on_tensor_device
 def token_logprobs_backward(hidden: torch.Tensor, w_vocab: torch.Tensor, tokens: torch.Tensor,
                             mask: Optional[torch.Tensor], lse: torch.Tensor, grad_logp: torch.Tensor, *,
                             grad_w: Optional[torch.Tensor] = None, accumulate_w: bool = False,
@@ -313,6 +335,7 @@ def _dev_2d(name, t, dtype, shape=None):
     return t
 
 
+@_on_tensor_device
 def select_constrained(a: torch.Tensor, b: Optional[torch.Tensor], mask: Optional[torch.Tensor], k: int, *,
                        lo: Optional[torch.Tensor] = None, hi: Optional[torch.Tensor] = None, min_gap: int = 0,
                        refill: bool = False):
@@ -344,6 +367,7 @@ def select_constrained(a: torch.Tensor, b: Optional[torch.Tensor], mask: Optiona
     return idx, score, count
 
 
+@_on_tensor_device
 def allocate_continuations(idx: torch.Tensor, count: torch.Tensor, alloc=(3, 4), fallback_pos: int = 0):
     """Continuation slots per root: returns (branch_pos [R, sum(alloc)], branch_rank [R, sum(alloc)])."""
     L = load_library()
@@ -362,6 +386,7 @@ def allocate_continuations(idx: torch.Tensor, count: torch.Tensor, alloc=(3, 4),
     return pos, rank
 
 
+@_on_tensor_device
 def group_advantages(rewards: torch.Tensor) -> torch.Tensor:
     """A = R - mean over each group (rows of rewards [n_groups, G], fp32)."""
     L = load_library()
@@ -372,6 +397,7 @@ def group_advantages(rewards: torch.Tensor) -> torch.Tensor:
     return adv
 
 
+@_on_tensor_device
 def policy_loss_grad(adv: torch.Tensor, traj: torch.Tensor, logp_new: torch.Tensor, logp_old: torch.Tensor, *,
                      loss_mask: Optional[torch.Tensor] = None, pos: Optional[torch.Tensor] = None,
                      start: Optional[torch.Tensor] = None, eps_low: float = 0.2, eps_high: float = 0.28,

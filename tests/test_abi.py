@@ -147,3 +147,17 @@ def test_group_construction_argument_errors(lib):
                                                                                 ctypes.c_void_p]
     assert pg(p, 4, p, p, None, p, p, None, 10, 0.2, 0.28, 1.0, p, None, None) == -1   # pos without start
     assert pg(p, 4, p, None, None, p, p, None, 10, -0.2, 0.28, 1.0, p, None, None) == -1
+
+
+def test_binding_rejects_host_tensors_before_any_launch():
+    import torch
+    import paper_2609_36864_amd as hdl
+    h = torch.zeros(4, 64, dtype=torch.bfloat16)
+    w = torch.zeros(10, 64, dtype=torch.bfloat16)
+    y = torch.zeros(4, dtype=torch.int32)
+    with pytest.raises(ValueError):
+        hdl.token_logprobs(h, w, y)
+    with pytest.raises(ValueError):
+        hdl.select_top_k(torch.zeros(2, 8), None, 2)
+    with pytest.raises(ValueError):
+        hdl.group_advantages(torch.zeros(2, 4))
