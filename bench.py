@@ -413,7 +413,8 @@ def bench_backward(args, w, hdl, dev) -> int:
                    "trained_tokens_per_step": n_scored},
         "roofline": {"bound": "mfma", "achieved": gemm_tflops, "peak": peak, "unit": "TFLOP/s",
                      "frac": gemm_tflops / peak, "traffic": None,
-                     "kernel": "gemm_nt_kernel (dH = G W, dW = G^T H; 55 % of the pass)",
+                     "kernel": f"gemm_kernel (dH = G W, dW = G^T H; "
+                               f"{100.0 * gemm_ms / args.steps / step_ms:.0f} % of the pass)",
                      "kernel_ms": gemm_launch_ms, "flops_per_launch": gemm_flops,
                      "gradient_mode_kernel": {"kernel_ms": grad_launch_ms, "achieved": grad_tflops,
                                               "frac": grad_tflops / peak},

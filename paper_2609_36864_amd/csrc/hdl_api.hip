@@ -329,16 +329,20 @@ int hdl_profile_read_kind(int kind, double* total_ms, int64_t* launches) {
 namespace {
 
 // How one hdl_token_logprobs_backward call is cut up.  Scored rows are taken
-// in chunks of `nc`; for each chunk the gradient with respect to the logits
-// G [nc][v_pad] (bf16) and its transpose exist at once, never more.
+// in chunks of `nc`; the gradient with respect to the logits, G [nc][v_pad]
+// (bf16), exists for one chunk at a time, never more.
 struct BwdPlan {
   int64_t nc, v_pad, n_chunks;
   int64_t splits, k_split;      // vocabulary split of the dH contraction
   hdl::LmheadPlan fwd;          // gradient-mode lm-head launches (nc rows)
-  size_t off_rows, off_count, off_wt, off_g, off_gt, off_ht, off_hpart, bytes;
+  size_t off_rows, off_count, off_g, off_hc, off_hpart, bytes;
 };
 
 constexpr int64_t kBwdChunkRows = 8192;
+// The GEMMs address a 256-row tile of G, or a 64-row K-slice of W, G or the
+// gathered hidden rows, with 32-bit byte offsets.
+constexpr int64_t kBwdMaxVocab = (int64_t{1} << 23) - 64;
+constexpr int64_t kBwdMaxD = int64_t{1} << 23;
 
 BwdPlan make_bwd_plan(int64_t n_rows, int64_t vocab, int64_t d) {
   BwdPlan p{};
@@ -361,27 +365,32 @@ BwdPlan make_bwd_plan(int64_t n_rows, int64_t vocab, int64_t d) {
   off = round_up(off + sizeof(int32_t) * static_cast<size_t>(n_rows), 256);
   p.off_count = off;
   off = round_up(off + sizeof(int32_t) * (64 + static_cast<size_t>((n_rows + 4095) / 4096)), 256);
-  p.off_wt = off;   // W^T [d][v_pad] bf16
-  off = round_up(off + 2 * static_cast<size_t>(d) * static_cast<size_t>(p.v_pad), 256);
   p.off_g = off;    // G [nc][v_pad] bf16
   off = round_up(off + 2 * static_cast<size_t>(p.nc) * static_cast<size_t>(p.v_pad), 256);
-  p.off_gt = off;   // G^T [v_pad][nc] bf16
-  off = round_up(off + 2 * static_cast<size_t>(p.nc) * static_cast<size_t>(p.v_pad), 256);
-  p.off_ht = off;   // chunk hidden rows transposed [d][nc] bf16
-  off = round_up(off + 2 * static_cast<size_t>(d) * static_cast<size_t>(p.nc), 256);
+  p.off_hc = off;   // the chunk's scored hidden rows, gathered [nc][d] bf16
+  off = round_up(off + 2 * static_cast<size_t>(p.nc) * static_cast<size_t>(d), 256);
   p.off_hpart = off;   // dH partial sums [splits][nc][d] fp32
   off = round_up(off + 4 * static_cast<size_t>(p.splits) * static_cast<size_t>(p.nc) * static_cast<size_t>(d), 256);
   p.bytes = off;
   return p;
 }
 
-hdl::GemmArgs gemm_args(const void* a, int64_t lda, const void* b, int64_t ldb, int64_t m, int64_t n, int64_t k,
-                        float* c, int64_t ldc) {
+// Arguments of C = sum_k A(m, k) B(n, k) with B stored with K as its row
+// (A too when a_krow).
+hdl::GemmArgs gemm_args(const void* a, int64_t lda, int a_krow, int64_t a_cols, int64_t a_krows, const void* b,
+                        int64_t ldb, int64_t b_cols, int64_t b_krows, int64_t m, int64_t n, int64_t k, float* c,
+                        int64_t ldc) {
   hdl::GemmArgs g{};
   g.a = a;
   g.lda = lda;
+  g.a_krow = a_krow;
+  g.a_cols = a_cols;
+  g.a_krows = a_krows;
   g.b = b;
   g.ldb = ldb;
+  g.b_krow = 1;
+  g.b_cols = b_cols;
+  g.b_krows = b_krows;
   g.m = m;
   g.n = n;
   g.k = k;
@@ -403,6 +412,7 @@ extern "C" {
 size_t hdl_token_logprobs_backward_workspace_size(int64_t n_rows, int64_t d, int64_t vocab, int dtype) {
   if (n_rows <= 0 || d <= 0 || vocab <= 0 || n_rows > INT32_MAX || vocab > INT32_MAX) return 0;
   if (dtype != HDL_BF16 || d % 8 != 0) return 0;
+  if (vocab > kBwdMaxVocab || d > kBwdMaxD) return 0;
   if (hdl::rows_per_launch(d, 2) < n_rows) return 0;
   return make_bwd_plan(n_rows, vocab, d).bytes;
 }
@@ -424,6 +434,9 @@ int hdl_token_logprobs_backward(const void* hidden, const void* w_vocab, const i
   if (dtype != HDL_BF16) return fail(HDL_ERR_UNSUPPORTED, "%s: only bf16 inputs are supported", fn);
   if (d % 8 != 0)
     return fail(HDL_ERR_UNSUPPORTED, "%s: d=%lld is not a multiple of 8", fn, static_cast<long long>(d));
+  if (vocab > kBwdMaxVocab || d > kBwdMaxD)
+    return fail(HDL_ERR_UNSUPPORTED, "%s: vocab must not exceed %lld and d %lld", fn,
+                static_cast<long long>(kBwdMaxVocab), static_cast<long long>(kBwdMaxD));
   if (hdl::rows_per_launch(d, 2) < n_rows)
     return fail(HDL_ERR_UNSUPPORTED, "%s: hidden states larger than 4 GiB", fn);
   if (!aligned(hidden, 16) || !aligned(w_vocab, 16) || !aligned(grad_hidden, 16) || !aligned(grad_w, 16))
@@ -439,26 +452,14 @@ int hdl_token_logprobs_backward(const void* hidden, const void* w_vocab, const i
   char* ws = static_cast<char*>(workspace);
   int32_t* rows = reinterpret_cast<int32_t*>(ws + plan.off_rows);
   int32_t* n_scored = reinterpret_cast<int32_t*>(ws + plan.off_count);
-  uint16_t* wt = reinterpret_cast<uint16_t*>(ws + plan.off_wt);
   uint16_t* g = reinterpret_cast<uint16_t*>(ws + plan.off_g);
-  uint16_t* gt = reinterpret_cast<uint16_t*>(ws + plan.off_gt);
-  uint16_t* ht = reinterpret_cast<uint16_t*>(ws + plan.off_ht);
+  uint16_t* hc = reinterpret_cast<uint16_t*>(ws + plan.off_hc);
   float* hpart = reinterpret_cast<float*>(ws + plan.off_hpart);
 
   hipError_t e = hdl::launch_compact(mask, n_rows, rows, n_scored, nullptr, nullptr, nullptr, s);
   if (e != hipSuccess) return hip_fail(e, "compaction launch");
   if ((e = hdl::launch_zero_masked_rows(mask, n_rows, d, grad_hidden, s)) != hipSuccess)
     return hip_fail(e, "row clearing launch");
-  hdl::TransposeArgs tw{};
-  tw.in = static_cast<const uint16_t*>(w_vocab);
-  tw.ld_in = d;
-  tw.r_cap = vocab;
-  tw.c_valid = d;
-  tw.out = wt;
-  tw.ld_out = plan.v_pad;
-  tw.out_rows = d;
-  if ((e = hdl::launch_transpose(tw, s)) != hipSuccess) return hip_fail(e, "transpose launch");
-
   for (int64_t c = 0; c < plan.n_chunks; ++c) {
     const int64_t base = c * plan.nc;
     // 1. G for this chunk's scored rows (logits recomputed tile by tile)
@@ -485,32 +486,13 @@ int hdl_token_logprobs_backward(const void* hidden, const void* w_vocab, const i
     if ((e = tg_.start(s)) != hipSuccess) return hip_fail(e, "timing event");
     if ((e = hdl::launch_lmhead_grad(a, plan.fwd.grid, s)) != hipSuccess) return hip_fail(e, "gradient kernel launch");
     if ((e = tg_.stop(HDL_PROFILE_GRAD, s)) != hipSuccess) return hip_fail(e, "timing event");
-    // 2. G^T and the chunk's hidden rows transposed, zero beyond the scored rows
-    hdl::TransposeArgs tg{};
-    tg.in = g;
-    tg.ld_in = plan.v_pad;
-    tg.dyn = n_scored;
-    tg.dyn_base = base;
-    tg.r_cap = plan.nc;
-    tg.c_valid = plan.v_pad;
-    tg.out = gt;
-    tg.ld_out = plan.nc;
-    tg.out_rows = plan.v_pad;
-    if ((e = hdl::launch_transpose(tg, s)) != hipSuccess) return hip_fail(e, "transpose launch");
-    hdl::TransposeArgs th{};
-    th.in = static_cast<const uint16_t*>(hidden);
-    th.ld_in = d;
-    th.map = rows + base;
-    th.dyn = n_scored;
-    th.dyn_base = base;
-    th.r_cap = plan.nc;
-    th.c_valid = d;
-    th.out = ht;
-    th.ld_out = plan.nc;
-    th.out_rows = d;
-    if ((e = hdl::launch_transpose(th, s)) != hipSuccess) return hip_fail(e, "transpose launch");
-    // 3. dH rows of the chunk: G W, split along the vocabulary, partials summed in order
-    hdl::GemmArgs gh = gemm_args(g, plan.v_pad, wt, plan.v_pad, plan.nc, d, plan.v_pad, hpart, d);
+    // 2. the chunk's scored hidden rows, gathered (zeros up to the next 64 rows)
+    if ((e = hdl::launch_gather_rows(static_cast<const uint16_t*>(hidden), d, rows + base, n_scored, base, plan.nc,
+                                     d, hc, s)) != hipSuccess)
+      return hip_fail(e, "row gather launch");
+    // 3. dH rows of the chunk: G W (W read as stored, K = vocabulary rows past
+    // V clamped: G is zero there), split along the vocabulary, partials summed in order
+    hdl::GemmArgs gh = gemm_args(g, plan.v_pad, 0, 0, 0, w_vocab, d, d, vocab, plan.nc, d, plan.v_pad, hpart, d);
     gh.dyn = n_scored;
     gh.dyn_base = base;
     gh.dyn_dim = 1;
@@ -519,20 +501,21 @@ int hdl_token_logprobs_backward(const void* hidden, const void* w_vocab, const i
     gh.c_split_stride = plan.nc * d;
     TimedLaunch th_;
     if ((e = th_.start(s)) != hipSuccess) return hip_fail(e, "timing event");
-    if ((e = hdl::launch_gemm_nt(gh, s)) != hipSuccess) return hip_fail(e, "GEMM launch");
+    if ((e = hdl::launch_gemm(gh, s)) != hipSuccess) return hip_fail(e, "GEMM launch");
     if ((e = th_.stop(HDL_PROFILE_GEMM, s)) != hipSuccess) return hip_fail(e, "timing event");
     if ((e = hdl::launch_splitk_scatter(hpart, plan.splits, plan.nc * d, d, rows + base, n_scored, base, plan.nc,
                                         grad_hidden, s)) != hipSuccess)
       return hip_fail(e, "split-K sum launch");
-    // 4. dW (+)= G^T H over the chunk's rows
-    hdl::GemmArgs gw = gemm_args(gt, plan.nc, ht, plan.nc, vocab, d, plan.nc, grad_w, d);
+    // 4. dW (+)= G^T H over the chunk's rows (both read with the row index as K)
+    hdl::GemmArgs gw = gemm_args(g, plan.v_pad, 1, plan.v_pad, plan.nc, hc, d, d, plan.nc, vocab, d, plan.nc,
+                                 grad_w, d);
     gw.dyn = n_scored;
     gw.dyn_base = base;
     gw.dyn_dim = 2;
     gw.beta = (c > 0 || accumulate_w) ? 1 : 0;
     TimedLaunch tw_;
     if ((e = tw_.start(s)) != hipSuccess) return hip_fail(e, "timing event");
-    if ((e = hdl::launch_gemm_nt(gw, s)) != hipSuccess) return hip_fail(e, "GEMM launch");
+    if ((e = hdl::launch_gemm(gw, s)) != hipSuccess) return hip_fail(e, "GEMM launch");
     if ((e = tw_.stop(HDL_PROFILE_GEMM, s)) != hipSuccess) return hip_fail(e, "timing event");
   }
   return HDL_OK;

@@ -55,21 +55,32 @@ struct LmheadArgs {
   int64_t row_base, row_cap;
   // Gradient mode (backward pass): instead of partial statistics, write
   // G[e][v] = g_e (1[v == y_e] - exp(z_ev - lse_e)) as bf16 for scored row e
-  // of this launch, columns v < g_cols (zero for v >= vocab).
+  // of this launch, columns v < g_cols (zero for v >= vocab), and zero rows
+  // for n <= e < round_up(n, 64).
   const float* lse_in;      // [n_rows] log-sum-exp from the forward pass
   const float* grad_in;     // [n_rows] upstream gradient of log p
   uint16_t* g_out;          // [row_cap][g_ld] bf16, or nullptr (statistics mode)
   int64_t g_ld, g_cols;
 };
 
-// Plain bf16 NT GEMM on the same 256 x 256 MFMA tile:
-//   C[s][m][n] (=|+=) sum_{k in split s} A[m][k] B[n][k]
-// A [M][lda] and B [N][ldb] are K-contiguous; K ranges are multiples of 64.
+// Plain bf16 GEMM on the same 256 x 256 MFMA tile:
+//   C[s][m][n] (=|+=) sum_{k in split s} A(m, k) B(n, k)
+// Each operand is stored either K-contiguous (row m of A holds A(m, 0..K);
+// the "row" layout) or with K as its row (row k of A holds A(0..M, k); the
+// "K-row" layout, read with transposing LDS loads), so G, W and the hidden
+// rows are all used as stored.  K ranges are multiples of 64.
 struct GemmArgs {
   const void* a;
   int64_t lda;
+  int a_krow;               // layout of A: 0 row, 1 K-row
+  // K-row layout only: stored columns (multiple of 8; reads past them are
+  // clamped) and stored rows (reads of K rows past them are clamped; the
+  // other operand must hold zeros at those K).
+  int64_t a_cols, a_krows;
   const void* b;
   int64_t ldb;
+  int b_krow;
+  int64_t b_cols, b_krows;
   int64_t m, n, k;          // sizes (upper bounds when a dimension is dynamic)
   // Dynamic dimension: dyn_dim 1 makes M = clamp(*dyn - dyn_base, 0, m);
   // dyn_dim 2 makes K = round_up(clamp(*dyn - dyn_base, 0, k), 64).
@@ -83,28 +94,17 @@ struct GemmArgs {
   int beta;                 // 0: store, 1: accumulate
 };
 
-// Transpose of a bf16 matrix with zero fill and an optional row gather:
-//   out[c][r] = (r < r_valid && c < c_valid) ? in[map ? map[r] : r][c] : 0
-// for c < out_rows and r < r_cols_written, where r_valid is
-// clamp(*dyn - dyn_base, 0, r_cap) when dyn is given (else r_cap) and only
-// columns r < round_up(r_valid, 64) are written.  c_valid % 8 == 0.
-struct TransposeArgs {
-  const uint16_t* in;
-  int64_t ld_in;
-  const int32_t* map;
-  const int32_t* dyn;
-  int64_t dyn_base, r_cap, c_valid;
-  uint16_t* out;
-  int64_t ld_out, out_rows;
-};
-
 hipError_t launch_compact(const uint8_t* mask, int64_t n_rows, int32_t* rows,
                           int32_t* n_scored, float* logp, float* lse, float* entropy,
                           hipStream_t stream);
 hipError_t launch_lmhead(const LmheadArgs& a, int64_t grid, bool bf16, hipStream_t stream);
 hipError_t launch_lmhead_grad(const LmheadArgs& a, int64_t grid, hipStream_t stream);
-hipError_t launch_gemm_nt(const GemmArgs& a, hipStream_t stream);
-hipError_t launch_transpose(const TransposeArgs& a, hipStream_t stream);
+// Supported layouts (a_krow, b_krow): (0, 1) and (1, 1).
+hipError_t launch_gemm(const GemmArgs& a, hipStream_t stream);
+// out[e][:] = e < n ? in[map[e]][:] : 0 for e < min(round_up(n, 64), cap), where
+// n = clamp(*dyn - dyn_base, 0, cap); out is [cap][d] bf16, d % 8 == 0.
+hipError_t launch_gather_rows(const uint16_t* in, int64_t ld_in, const int32_t* map, const int32_t* dyn,
+                              int64_t dyn_base, int64_t cap, int64_t d, uint16_t* out, hipStream_t stream);
 // dh[map[e]][j] = sum_s part[s][e][j] for e < clamp(*dyn - dyn_base, 0, cap)
 hipError_t launch_splitk_scatter(const float* part, int64_t splits, int64_t split_stride, int64_t d,
                                  const int32_t* map, const int32_t* dyn, int64_t dyn_base, int64_t cap,

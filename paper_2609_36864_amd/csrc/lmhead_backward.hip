@@ -11,11 +11,14 @@
 // rows x vocabulary tensor never exists whole) by the fused lm-head kernel in
 // its gradient mode, which recomputes the logits tile by tile.  The two
 // contractions are plain bf16 GEMMs on the same 256 x 256 MFMA tile as the
-// forward kernel (gemm_nt_kernel below); both of their operands must be
-// contiguous along the contracted index, so G, W and the chunk's hidden rows
-// are also written transposed (transpose_kernel).  dH is split along the
-// vocabulary for parallelism and its partial sums are added in a fixed order
-// (splitk_scatter_kernel): the whole pass is deterministic.
+// forward kernel (gemm_kernel below).  Each operand is read as stored: G is
+// K-contiguous for dH and has the contracted index as its row for dW, W and
+// the chunk's hidden rows (gathered into a dense block by gather_rows_kernel)
+// have it as their row; those operands are staged in LDS as stored and turned
+// into MFMA fragments by gfx950's transposing LDS reads, so nothing is
+// transposed in memory.  dH is split along the vocabulary for parallelism and
+// its partial sums are added in a fixed order (splitk_scatter_kernel): the
+// whole pass is deterministic.
 #include "tile_common.h"
 
 namespace hdl {
@@ -24,12 +27,111 @@ namespace {
 using namespace tile;
 
 constexpr int kGemmSliceK = 8 * kChunks;   // bf16 elements per K-slice
+// K-row operand tiles: a K-slice is 64 stored rows of kTileV bf16 (512 bytes,
+// 32 chunks of 16 bytes), the same 32 KB as a row-layout slice.
+constexpr int kKRowChunks = kTileV * 2 / 16;
+static_assert(kGemmSliceK * kKRowChunks == kSlots, "K-row slice must fill one operand stage");
+static_assert(2 * kKRowChunks == 64, "one DMA block must hold two stored K rows");
 
-// C[s][m][n] (=|+=) sum_k A[m][k] B[n][k] over the K range of split s, for
+typedef short i16x4_t __attribute__((ext_vector_type(4)));
+
+// XOR pattern of the 16-byte chunks of K-row r.  A transposing read by 16
+// lanes touches 32 bytes (two chunks) in each of 4 consecutive rows, and 32
+// lanes touch 64 bytes in each of those rows; with 512-byte rows every row
+// starts on the same bank, so the pattern must give the 4 rows distinct
+// 32-byte bank positions within 128 bytes (bits 1-2 of the chunk index) and
+// distinct 64-byte positions within 256 bytes (bits 2-3): (j0, j1) = the two
+// low bits of r map to bits (2, 1) and bit 3 takes j0 ^ j1.
+__device__ __forceinline__ int krow_xor(int r) {
+  const int j0 = r & 1, j1 = (r >> 1) & 1;
+  return 2 * j1 + 4 * j0 + 8 * (j0 ^ j1);
+}
+
+// Per-lane DMA and fragment addressing of one operand of the tile.
+template <bool KROW>
+struct Operand {
+  uint32_t off[kBlocksPerWave];   // per-lane byte offset of each DMA block (row layout: final)
+  uint32_t colb[kBlocksPerWave];  // K-row layout: per-lane column byte offset of each DMA block
+  uint64_t tile;                  // uniform base of the tile
+  int64_t ld2;                    // bytes per stored row
+  int64_t krows;                  // K-row layout: stored rows
+  uint32_t frag[4];               // K-row layout: per-lane LDS byte offset of each 32-wide MFMA block
+
+  // row layout: the tile's rows t0 .. t0+255 (clamped to `rows`), K-contiguous.
+  // K-row layout: the tile's columns t0 .. t0+255 (clamped to `cols`) of every
+  // stored row.
+  __device__ __forceinline__ void init(const void* ptr, int64_t ld, int64_t t0, int64_t rows, int64_t cols,
+                                       int64_t krows_, int wave, int lane, int nblk, int blk0) {
+    ld2 = ld * 2;
+    krows = krows_;
+    if (!KROW) {
+      tile = reinterpret_cast<uint64_t>(ptr) + static_cast<uint64_t>(t0 * ld2);
+      const int lrow = lane / kChunks;
+#pragma unroll
+      for (int i = 0; i < kBlocksPerWave; ++i) {
+        const int r = wave * (kTileV / kWaves) + i * kBlockRows + lrow;
+        int64_t row = t0 + r;
+        row = row < rows ? row : rows - 1;
+        const int chunk = (lane % kChunks) ^ row_xor((wave * kBlocksPerWave + i) * kBlockRows + lrow);
+        off[i] = static_cast<uint32_t>((row - t0) * ld2 + chunk * 16);
+      }
+    } else {
+      tile = reinterpret_cast<uint64_t>(ptr) + static_cast<uint64_t>(t0 * 2);
+#pragma unroll
+      for (int i = 0; i < kBlocksPerWave; ++i) {
+        const int r = 2 * (wave * kBlocksPerWave + i) + (lane >> 5);   // stored row within the slice
+        const int chunk = (lane & 31) ^ krow_xor(r);
+        int64_t c = t0 + 8 * chunk;
+        c = c < cols - 8 ? c : cols - 8;
+        colb[i] = static_cast<uint32_t>((c - t0) * 2);
+      }
+      // fragment reads: lane l of a 16-lane group reads stored row 4 j + l / 4
+      // (j: which half of the 8 K values) at columns 4 (l % 4) .. +3 of its
+      // group's 16 columns; lanes 32-63 take K values 8-15 of the sub-step
+      const int a = lane & 15, gi = (lane >> 4) & 1, half = lane >> 5;
+#pragma unroll
+      for (int bk = 0; bk < nblk; ++bk) {
+        const int c = (((blk0 + bk * 32) >> 3) + 2 * gi + ((a & 3) >> 1)) ^ krow_xor(a >> 2);
+        frag[bk] = static_cast<uint32_t>(((a >> 2) + 8 * half) * (kKRowChunks * 16) + c * 16 + (a & 1) * 8);
+      }
+    }
+  }
+  // uniform address of K-slice starting at element k
+  __device__ __forceinline__ uint64_t slice_base(int64_t k) const {
+    return KROW ? tile + static_cast<uint64_t>(k * ld2) : tile + static_cast<uint64_t>(k * 2);
+  }
+  // last stored row of the K-slice starting at element k, relative to it
+  // (>= 0: every slice starts at a stored row; 63 when the slice is whole)
+  __device__ __forceinline__ int slice_rmax(int64_t k) const {
+    const int64_t r = krows - 1 - k;
+    return r < kGemmSliceK - 1 ? static_cast<int>(r) : kGemmSliceK - 1;
+  }
+  // per-lane offset of DMA block i of a K-slice whose last stored row is rmax
+  __device__ __forceinline__ uint32_t block_off(int i, int rmax, int wave, int lane) const {
+    if (!KROW) return off[i];
+    const int r = 2 * (wave * kBlocksPerWave + i) + (lane >> 5);
+    const int rr = r < rmax ? r : rmax;
+    return static_cast<uint32_t>(rr) * static_cast<uint32_t>(ld2) + colb[i];
+  }
+};
+
+// 16 bytes of an MFMA fragment (8 consecutive K values of one column) from a
+// K-row LDS tile: two transposing 8-byte reads, 4 K values each.
+__device__ __forceinline__ uint4 krow_frag(const char __attribute__((address_space(3)))* base, uint32_t off) {
+  typedef __attribute__((address_space(3))) i16x4_t lds_i16x4;
+  const i16x4_t lo = __builtin_amdgcn_ds_read_tr16_b64_v4i16((lds_i16x4*)(base + off));
+  const i16x4_t hi = __builtin_amdgcn_ds_read_tr16_b64_v4i16((lds_i16x4*)(base + off + 4 * kKRowChunks * 16));
+  const uint2 l = __builtin_bit_cast(uint2, lo), h = __builtin_bit_cast(uint2, hi);
+  return make_uint4(l.x, l.y, h.x, h.y);
+}
+
+// C[s][m][n] (=|+=) sum_k A(m, k) B(n, k) over the K range of split s, for
 // one 256 x 256 tile of C per workgroup.  Same data path as the fused
-// kernel: K-slices of 128 bytes per row stream into a 2-stage LDS ring by
-// direct DMA; eight waves each own 128 x 64 of the tile as 4 x 2 MFMA blocks.
-__global__ __launch_bounds__(kThreads, 1) void gemm_nt_kernel(GemmArgs p) {
+// kernel: K-slices of 64 K values stream into a 2-stage LDS ring by direct
+// DMA; eight waves each own 128 x 64 of the tile as 4 x 2 MFMA blocks.
+// AK / BK: operand stored with K as its row.
+template <bool AK, bool BK>
+__global__ __launch_bounds__(kThreads, 1) void gemm_kernel(GemmArgs p) {
   using M = Mma<true>;
   static_assert(kWaves == 8 && kNB == 2, "8-wave tile layout assumed");
   __shared__ uint4 lds[kStages][2][kSlots];   // [stage][0 = A, 1 = B]
@@ -83,50 +185,49 @@ __global__ __launch_bounds__(kThreads, 1) void gemm_nt_kernel(GemmArgs p) {
       for (int q = 0; q < 16; ++q) acc[bm][bn][q] = 0.f;
 
   if (n_iter > 0) {
-    // ---- DMA addressing (tile-relative 32-bit offsets, uniform 64-bit base)
-    const int lrow = lane / kChunks;
-    auto dma_chunk = [&](int i) {
-      const int row = (wave * kBlocksPerWave + i) * kBlockRows + lrow;
-      return (lane % kChunks) ^ row_xor(row);
-    };
-    const int64_t a_row_bytes = p.lda * 2, b_row_bytes = p.ldb * 2;
-    uint32_t aoff[kBlocksPerWave], boff[kBlocksPerWave];
-#pragma unroll
-    for (int i = 0; i < kBlocksPerWave; ++i) {
-      const int r = wave * (kTileV / kWaves) + i * kBlockRows + lrow;
-      int64_t ra = tm * kTileV + r;
-      ra = ra < m_valid ? ra : m_valid - 1;
-      int64_t rb = tn * kTileN + r;
-      rb = rb < p.n ? rb : p.n - 1;
-      aoff[i] = static_cast<uint32_t>((ra - tm * kTileV) * a_row_bytes + dma_chunk(i) * 16);
-      boff[i] = static_cast<uint32_t>((rb - tn * kTileN) * b_row_bytes + dma_chunk(i) * 16);
-    }
-    const uint64_t atile = reinterpret_cast<uint64_t>(p.a) + static_cast<uint64_t>(tm * kTileV * a_row_bytes);
-    const uint64_t btile = reinterpret_cast<uint64_t>(p.b) + static_cast<uint64_t>(tn * kTileN * b_row_bytes);
+    Operand<AK> A;
+    Operand<BK> B;
+    A.init(p.a, p.lda, tm * kTileV, m_valid, p.a_cols, p.a_krows, wave, lane, 4, wm * 128);
+    B.init(p.b, p.ldb, tn * kTileN, p.n, p.b_cols, p.b_krows, wave, lane, kNB, wn * kWaveN);
     const uint32_t lds_base = static_cast<uint32_t>(
         reinterpret_cast<size_t>((__attribute__((address_space(3))) uint4*)(&lds[0][0][0])));
+    const char __attribute__((address_space(3)))* lds_bytes =
+        (const char __attribute__((address_space(3)))*)(&lds[0][0][0]);
     auto lds_addr = [&](int stage, int op, int block) -> uint32_t {
       return __builtin_amdgcn_readfirstlane(
           lds_base + static_cast<uint32_t>(((stage * 2 + op) * kSlots + block * 64) * 16));
     };
-    uint32_t issue_kbytes = 0;
-    int issue_stage = 0;
+    int issue_stage = 0, a_rmax = 0, b_rmax = 0;
+    uint64_t a_slice = 0, b_slice = 0;
     auto prep_issue = [&](int slice) {
       issue_stage = slice % kStages;
-      issue_kbytes = static_cast<uint32_t>((k0 + static_cast<int64_t>(slice) * kGemmSliceK) * 2);
+      const int64_t k = k0 + static_cast<int64_t>(slice) * kGemmSliceK;
+      a_slice = A.slice_base(k);
+      b_slice = B.slice_base(k);
+      if (AK) a_rmax = A.slice_rmax(k);
+      if (BK) b_rmax = B.slice_rmax(k);
     };
     auto issue_one = [&](int jj) {
       const int i = jj % kBlocksPerWave;
-      const bool is_a = jj < kBlocksPerWave;
-      dma16((is_a ? atile : btile) + issue_kbytes, is_a ? aoff[i] : boff[i],
-            lds_addr(issue_stage, is_a ? 0 : 1, wave * kBlocksPerWave + i));
+      if (jj < kBlocksPerWave)
+        dma16(a_slice, A.block_off(i, a_rmax, wave, lane), lds_addr(issue_stage, 0, wave * kBlocksPerWave + i));
+      else
+        dma16(b_slice, B.block_off(i, b_rmax, wave, lane), lds_addr(issue_stage, 1, wave * kBlocksPerWave + i));
     };
     auto load_frags = [&](int slice, int kk, uint4 (&fa)[4], uint4 (&fb)[kNB]) {
       const int stage = slice % kStages;
+      // K-row tiles: sub-step kk covers stored rows 16 kk .. 16 kk + 15
+      const uint32_t ks = static_cast<uint32_t>(kk * 16 * kKRowChunks * 16);
 #pragma unroll
-      for (int bm = 0; bm < 4; ++bm) fa[bm] = lds[stage][0][swz(wm * 128 + bm * 32 + col, kk * 2 + half)];
+      for (int bm = 0; bm < 4; ++bm) {
+        if (AK) fa[bm] = krow_frag(lds_bytes + (stage * 2 + 0) * kSlots * 16, A.frag[bm] + ks);
+        else fa[bm] = lds[stage][0][swz(wm * 128 + bm * 32 + col, kk * 2 + half)];
+      }
 #pragma unroll
-      for (int bn = 0; bn < kNB; ++bn) fb[bn] = lds[stage][1][swz(wn * kWaveN + bn * 32 + col, kk * 2 + half)];
+      for (int bn = 0; bn < kNB; ++bn) {
+        if (BK) fb[bn] = krow_frag(lds_bytes + (stage * 2 + 1) * kSlots * 16, B.frag[bn] + ks);
+        else fb[bn] = lds[stage][1][swz(wn * kWaveN + bn * 32 + col, kk * 2 + half)];
+      }
     };
 
     const int n_pre = n_iter < kStages ? n_iter : kStages;
@@ -189,39 +290,23 @@ __global__ __launch_bounds__(kThreads, 1) void gemm_nt_kernel(GemmArgs p) {
   }
 }
 
-// 64 x 64 tiles through LDS: coalesced 16-byte reads of input rows and
-// 16-byte writes of output rows.
-__global__ __launch_bounds__(256) void transpose_kernel(TransposeArgs p) {
-  __shared__ __align__(16) uint16_t t[64][72];   // [input row][input column], rows padded to 144 bytes
-  int64_t r_valid = p.r_cap;
-  if (p.dyn) {
-    r_valid = *p.dyn - p.dyn_base;
-    r_valid = r_valid < 0 ? 0 : (r_valid > p.r_cap ? p.r_cap : r_valid);
-  }
-  const int64_t r_end = (r_valid + 63) / 64 * 64;
-  const int64_t r0 = static_cast<int64_t>(blockIdx.x) * 64;
-  const int64_t c0 = static_cast<int64_t>(blockIdx.y) * 64;
-  if (r0 >= r_end || c0 >= p.out_rows) return;
-  for (int q = threadIdx.x; q < 512; q += 256) {
-    const int i = q >> 3, cc = (q & 7) * 8;
-    const int64_t r = r0 + i, c = c0 + cc;
-    uint4 v = make_uint4(0, 0, 0, 0);
-    if (r < r_valid && c < p.c_valid) {
-      const int64_t src = p.map ? p.map[r] : r;
-      v = *reinterpret_cast<const uint4*>(p.in + src * p.ld_in + c);
-    }
-    *reinterpret_cast<uint4*>(&t[i][cc]) = v;
-  }
-  __syncthreads();
-  for (int q = threadIdx.x; q < 512; q += 256) {
-    const int i = q >> 3, rr = (q & 7) * 8;
-    if (c0 + i >= p.out_rows) continue;
-    uint32_t w[4];
-#pragma unroll
-    for (int u = 0; u < 4; ++u)
-      w[u] = static_cast<uint32_t>(t[rr + 2 * u][i]) | (static_cast<uint32_t>(t[rr + 2 * u + 1][i]) << 16);
-    *reinterpret_cast<uint4*>(p.out + (c0 + i) * p.ld_out + r0 + rr) = make_uint4(w[0], w[1], w[2], w[3]);
-  }
+// out[e][:] = in[map[e]][:] for the e < n scored rows of the chunk, zeros for
+// n <= e < round_up(n, 64): the dense K-row operand of dW = G^T H.
+__global__ __launch_bounds__(256) void gather_rows_kernel(const uint16_t* __restrict__ in, int64_t ld_in,
+                                                          const int32_t* __restrict__ map,
+                                                          const int32_t* __restrict__ dyn, int64_t dyn_base,
+                                                          int64_t cap, int64_t d, uint16_t* __restrict__ out) {
+  int64_t n = *dyn - dyn_base;
+  n = n < 0 ? 0 : (n > cap ? cap : n);
+  int64_t n_pad = (n + 63) / 64 * 64;
+  n_pad = n_pad < cap ? n_pad : cap;
+  const int64_t e = blockIdx.y;
+  if (e >= n_pad) return;
+  const int64_t j = (static_cast<int64_t>(blockIdx.x) * 256 + threadIdx.x) * 8;
+  if (j >= d) return;
+  uint4 v = make_uint4(0, 0, 0, 0);
+  if (e < n) v = *reinterpret_cast<const uint4*>(in + static_cast<int64_t>(map[e]) * ld_in + j);
+  *reinterpret_cast<uint4*>(out + e * d + j) = v;
 }
 
 // dh[map[e]][j] = sum over splits s (in order) of part[s][e][j].
@@ -255,20 +340,27 @@ __global__ __launch_bounds__(256) void zero_masked_rows_kernel(const uint8_t* __
 
 }  // namespace
 
-hipError_t launch_gemm_nt(const GemmArgs& a, hipStream_t stream) {
+hipError_t launch_gemm(const GemmArgs& a, hipStream_t stream) {
   const int64_t per_group = a.gm * a.gn;
   const int64_t groups = ((a.tiles_m + a.gm - 1) / a.gm) * ((a.tiles_n + a.gn - 1) / a.gn) * a.splits;
   const int64_t grid = (groups + kNumXcd - 1) / kNumXcd * kNumXcd * per_group;
   if (grid <= 0) return hipSuccess;
-  hipLaunchKernelGGL(gemm_nt_kernel, dim3(static_cast<unsigned>(grid)), dim3(kThreads), 0, stream, a);
+  const dim3 g(static_cast<unsigned>(grid)), blk(kThreads);
+  if (!a.a_krow && a.b_krow)
+    hipLaunchKernelGGL((gemm_kernel<false, true>), g, blk, 0, stream, a);
+  else if (a.a_krow && a.b_krow)
+    hipLaunchKernelGGL((gemm_kernel<true, true>), g, blk, 0, stream, a);
+  else
+    return hipErrorInvalidValue;
   return hipGetLastError();
 }
 
-hipError_t launch_transpose(const TransposeArgs& a, hipStream_t stream) {
-  const int64_t gx = (a.r_cap + 63) / 64, gy = (a.out_rows + 63) / 64;
-  if (gx <= 0 || gy <= 0) return hipSuccess;
-  hipLaunchKernelGGL(transpose_kernel, dim3(static_cast<unsigned>(gx), static_cast<unsigned>(gy)), dim3(256), 0,
-                     stream, a);
+hipError_t launch_gather_rows(const uint16_t* in, int64_t ld_in, const int32_t* map, const int32_t* dyn,
+                              int64_t dyn_base, int64_t cap, int64_t d, uint16_t* out, hipStream_t stream) {
+  const int64_t gx = (d / 8 + 255) / 256;
+  if (gx <= 0 || cap <= 0) return hipSuccess;
+  hipLaunchKernelGGL(gather_rows_kernel, dim3(static_cast<unsigned>(gx), static_cast<unsigned>(cap)), dim3(256), 0,
+                     stream, in, ld_in, map, dyn, dyn_base, cap, d, out);
   return hipGetLastError();
 }
 

@@ -85,7 +85,9 @@ __device__ __forceinline__ void combine(float& m, float& s, float& z, float& t, 
 //                baseline);
 //   kEpiGrad:    the gradient of log p with respect to the logits,
 //                g (1[v == y] - exp(z - lse)), written as bf16 (backward pass;
-//                lse comes from the forward pass).
+//                lse comes from the forward pass), with zero rows up to the
+//                next multiple of 64 rows so that a contraction over rows
+//                can run in whole 64-row K-slices.
 constexpr int kEpiStats = 0, kEpiEntropy = 1, kEpiGrad = 2;
 
 template <bool BF16, bool KTAIL, int EPI>
@@ -121,6 +123,7 @@ __global__ __launch_bounds__(kThreads, 1) void lmhead_logprob_kernel(LmheadArgs 
   int64_t n_s = *p.n_scored - p.row_base;
   n_s = n_s < 0 ? 0 : (n_s > p.row_cap ? p.row_cap : n_s);
   const int64_t n_rt = (n_s + kTileN - 1) / kTileN;
+  const int64_t n_s_pad = (n_s + 63) / 64 * 64;   // gradient mode: rows written (row_cap % 64 == 0)
   if (rt >= n_rt || ch >= p.n_ch) return;
 
   const int64_t vt0 = ch * p.tpc;
@@ -143,6 +146,8 @@ __global__ __launch_bounds__(kThreads, 1) void lmhead_logprob_kernel(LmheadArgs 
     const int row = p.rows[e];
     tok[bn] = p.tokens[row];
     if (GRAD) {
+      // no indicator term for a token outside [0, V): padding columns of G stay 0
+      tok[bn] = (tok[bn] >= 0 && tok[bn] < V) ? tok[bn] : -1;
       g_lse[bn] = p.lse_in[row] * kLog2e;
       g_up[bn] = p.grad_in[row];
     }
@@ -341,6 +346,7 @@ __global__ __launch_bounds__(kThreads, 1) void lmhead_logprob_kernel(LmheadArgs 
 #pragma unroll
     for (int bn = 0; bn < kNB; ++bn) {
       const int64_t e = rt * kTileN + wn * kWaveN + bn * 32 + col;
+      const bool live = e < n_s;   // rows n_s .. round_up(n_s, 64) - 1 are written as zeros
       uint16_t* grow = p.g_out + e * p.g_ld;
 #pragma unroll
       for (int bm = 0; bm < 4; ++bm) {
@@ -354,7 +360,7 @@ __global__ __launch_bounds__(kThreads, 1) void lmhead_logprob_kernel(LmheadArgs 
 #pragma unroll
             for (int u = 0; u < 2; ++u) {
               const float pv = fast_exp2(__builtin_fmaf(acc[bm][bn][jr * 4 + r + u], kLog2e, -g_lse[bn]));
-              gv[u] = (v + u == tok[bn]) ? g_up[bn] * (1.f - pv) : -g_up[bn] * pv;
+              gv[u] = !live ? 0.f : (v + u == tok[bn]) ? g_up[bn] * (1.f - pv) : -g_up[bn] * pv;
             }
             pk[jr][r / 2] = static_cast<uint32_t>(__builtin_bit_cast(uint16_t, static_cast<__bf16>(gv[0]))) |
                             (static_cast<uint32_t>(__builtin_bit_cast(uint16_t, static_cast<__bf16>(gv[1]))) << 16);
@@ -371,7 +377,7 @@ __global__ __launch_bounds__(kThreads, 1) void lmhead_logprob_kernel(LmheadArgs 
         const uint4 hi = half == 0 ? make_uint4(pk[1][0], pk[1][1], rv[2], rv[3])
                                    : make_uint4(rv[2], rv[3], pk[3][0], pk[3][1]);
         const int64_t v16 = vbase + bm * 32 + 16 * half;   // first of this lane's 16 entries
-        if (e < n_s && v16 < p.g_cols) {
+        if (e < n_s_pad && v16 < p.g_cols) {
           *reinterpret_cast<uint4*>(grow + v16) = lo;
           *reinterpret_cast<uint4*>(grow + v16 + 8) = hi;
         }

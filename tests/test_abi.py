@@ -98,10 +98,13 @@ def test_backward_workspace_and_argument_errors(lib):
     ws = lib.hdl_token_logprobs_backward_workspace_size
     ws.restype = ctypes.c_size_t
     ws.argtypes = [ctypes.c_int64, ctypes.c_int64, ctypes.c_int64, ctypes.c_int]
-    # one chunk of G and its transpose dominate: 4 * rows * round_up(V, 64) bytes
+    # one chunk of G dominates: 2 * round_up(rows, 256) * round_up(V, 64) bytes,
+    # plus the gathered hidden rows (2 * 1024 * d) and the dH partials (4 * splits * 1024 * d)
     n, d, V = 1000, 64, 1000
     size = ws(n, d, V, 1)
-    assert size >= 4 * 1024 * 1024 and size < 4 * 1024 * 1024 + 8 * 1024 * 1024
+    assert size >= 2 * 1024 * 1024 + 2 * 1024 * d and size < 2 * 1024 * 1024 + 40 * 1024 * d
+    assert ws(n, d, (1 << 23) - 64, 1) > 0 and ws(n, d, (1 << 23) - 63, 1) == 0   # vocabulary limit
+    assert ws(n, (1 << 23) + 8, V, 1) == 0
     assert ws(n, d, V, 0) == 0          # fp32 inputs are not supported
     assert ws(n, 12, V, 1) == 0         # d not a multiple of 8
     assert ws(0, d, V, 1) == 0
