@@ -160,10 +160,10 @@ int hdl_select_top_k(const float* values, const uint8_t* mask, int64_t n_roots, 
 /*
  * Bytes of device workspace hdl_token_logprobs_backward needs for these sizes
  * (0 if the sizes are invalid or unsupported).  Dominated by one chunk's
- * logit gradient, 2 * min(round_up(n_rows, 256), 8192) * round_up(vocab, 64)
- * bytes (2.5 GB for 8192 rows and a 151,936-token vocabulary), plus the
- * chunk's gathered hidden rows and the split partial sums of its dH rows
- * (about 0.17 GB at d = 2048).
+ * logit gradient, 2 * min(round_up(n_rows, 256), 32768) * round_up(vocab, 64)
+ * bytes (10 GB for 32768 rows and a 151,936-token vocabulary), plus the
+ * chunk's gathered hidden rows and the partial sums of its dH rows (about
+ * 0.4 GB for 32768 rows at d = 2048).
  */
 size_t hdl_token_logprobs_backward_workspace_size(int64_t n_rows, int64_t d, int64_t vocab,
                                                   int dtype);
@@ -178,12 +178,12 @@ size_t hdl_token_logprobs_backward_workspace_size(int64_t n_rows, int64_t d, int
  *     dL/dW_v  = sum_n G[n][v] h_n                   -> grad_w
  *
  * The logits are recomputed tile by tile from hidden and w_vocab; G exists
- * only for one chunk of at most 8192 scored rows at a time, as bf16; the two
+ * only for one chunk of at most 32768 scored rows at a time, as bf16; the two
  * contractions run on bf16 MFMA tiles with fp32 accumulation.
  *
  *  hidden, w_vocab, tokens, mask, n_rows, d, vocab: as for hdl_token_logprobs;
  *               dtype must be HDL_BF16.  Hidden states must not exceed 4 GiB,
- *               vocab must not exceed 2^23 - 64 and d 2^23
+ *               vocab must not exceed 2^30 and d 2^23
  *               (HDL_ERR_UNSUPPORTED otherwise).
  *  lse          [n_rows] fp32: the log-sum-exp hdl_token_logprobs returned
  *               for the same inputs (read for scored rows only).

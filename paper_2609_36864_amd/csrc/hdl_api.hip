@@ -338,10 +338,10 @@ struct BwdPlan {
   size_t off_rows, off_count, off_g, off_hc, off_hpart, bytes;
 };
 
-constexpr int64_t kBwdChunkRows = 8192;
-// The GEMMs address a 256-row tile of G, or a 64-row K-slice of W, G or the
-// gathered hidden rows, with 32-bit byte offsets.
-constexpr int64_t kBwdMaxVocab = (int64_t{1} << 23) - 64;
+constexpr int64_t kBwdChunkRows = 32768;
+// The GEMMs address a 64-row K-slice of W or of the gathered hidden rows
+// with 32-bit byte offsets; vocabulary indices stay well inside int32.
+constexpr int64_t kBwdMaxVocab = int64_t{1} << 30;
 constexpr int64_t kBwdMaxD = int64_t{1} << 23;
 
 BwdPlan make_bwd_plan(int64_t n_rows, int64_t vocab, int64_t d) {
@@ -365,7 +365,7 @@ BwdPlan make_bwd_plan(int64_t n_rows, int64_t vocab, int64_t d) {
   off = round_up(off + sizeof(int32_t) * static_cast<size_t>(n_rows), 256);
   p.off_count = off;
   off = round_up(off + sizeof(int32_t) * (64 + static_cast<size_t>((n_rows + 4095) / 4096)), 256);
-  p.off_g = off;    // G [nc][v_pad] bf16
+  p.off_g = off;    // G chunk-major [v_pad / 8][nc][8] bf16
   off = round_up(off + 2 * static_cast<size_t>(p.nc) * static_cast<size_t>(p.v_pad), 256);
   p.off_hc = off;   // the chunk's scored hidden rows, gathered [nc][d] bf16
   off = round_up(off + 2 * static_cast<size_t>(p.nc) * static_cast<size_t>(d), 256);
@@ -375,20 +375,20 @@ BwdPlan make_bwd_plan(int64_t n_rows, int64_t vocab, int64_t d) {
   return p;
 }
 
-// Arguments of C = sum_k A(m, k) B(n, k) with B stored with K as its row
-// (A too when a_krow).
-hdl::GemmArgs gemm_args(const void* a, int64_t lda, int a_krow, int64_t a_cols, int64_t a_krows, const void* b,
+// Arguments of C = sum_k A(m, k) B(n, k): A is the chunk-major logit
+// gradient (layout a_layout), B is stored with K as its row.
+hdl::GemmArgs gemm_args(const void* a, int64_t lda, int a_layout, int64_t a_cols, int64_t a_krows, const void* b,
                         int64_t ldb, int64_t b_cols, int64_t b_krows, int64_t m, int64_t n, int64_t k, float* c,
                         int64_t ldc) {
   hdl::GemmArgs g{};
   g.a = a;
   g.lda = lda;
-  g.a_krow = a_krow;
+  g.a_layout = a_layout;
   g.a_cols = a_cols;
   g.a_krows = a_krows;
   g.b = b;
   g.ldb = ldb;
-  g.b_krow = 1;
+  g.b_layout = hdl::kLayoutKRow;
   g.b_cols = b_cols;
   g.b_krows = b_krows;
   g.m = m;
@@ -480,7 +480,7 @@ int hdl_token_logprobs_backward(const void* hidden, const void* w_vocab, const i
     a.lse_in = lse;
     a.grad_in = grad_logp;
     a.g_out = g;
-    a.g_ld = plan.v_pad;
+    a.g_ld = plan.nc;   // chunk-major: nc rows per 8-column plane
     a.g_cols = plan.v_pad;
     TimedLaunch tg_;
     if ((e = tg_.start(s)) != hipSuccess) return hip_fail(e, "timing event");
@@ -492,7 +492,8 @@ int hdl_token_logprobs_backward(const void* hidden, const void* w_vocab, const i
       return hip_fail(e, "row gather launch");
     // 3. dH rows of the chunk: G W (W read as stored, K = vocabulary rows past
     // V clamped: G is zero there), split along the vocabulary, partials summed in order
-    hdl::GemmArgs gh = gemm_args(g, plan.v_pad, 0, 0, 0, w_vocab, d, d, vocab, plan.nc, d, plan.v_pad, hpart, d);
+    hdl::GemmArgs gh = gemm_args(g, plan.nc, hdl::kLayoutCmRow, 0, 0, w_vocab, d, d, vocab, plan.nc, d, plan.v_pad,
+                                 hpart, d);
     gh.dyn = n_scored;
     gh.dyn_base = base;
     gh.dyn_dim = 1;
@@ -507,8 +508,8 @@ int hdl_token_logprobs_backward(const void* hidden, const void* w_vocab, const i
                                         grad_hidden, s)) != hipSuccess)
       return hip_fail(e, "split-K sum launch");
     // 4. dW (+)= G^T H over the chunk's rows (both read with the row index as K)
-    hdl::GemmArgs gw = gemm_args(g, plan.v_pad, 1, plan.v_pad, plan.nc, hc, d, d, plan.nc, vocab, d, plan.nc,
-                                 grad_w, d);
+    hdl::GemmArgs gw = gemm_args(g, plan.nc, hdl::kLayoutCmKRow, plan.v_pad, plan.nc, hc, d, d, plan.nc, vocab, d,
+                                 plan.nc, grad_w, d);
     gw.dyn = n_scored;
     gw.dyn_base = base;
     gw.dyn_dim = 2;

@@ -56,30 +56,37 @@ struct LmheadArgs {
   // Gradient mode (backward pass): instead of partial statistics, write
   // G[e][v] = g_e (1[v == y_e] - exp(z_ev - lse_e)) as bf16 for scored row e
   // of this launch, columns v < g_cols (zero for v >= vocab), and zero rows
-  // for n <= e < round_up(n, 64).
+  // for n <= e < round_up(n, 64).  G is stored chunk-major: the 8 entries
+  // v = 8c .. 8c+7 of row e are the 16 bytes at element (c * g_ld + e) * 8,
+  // so consecutive rows' chunks are adjacent (g_ld >= row_cap).
   const float* lse_in;      // [n_rows] log-sum-exp from the forward pass
   const float* grad_in;     // [n_rows] upstream gradient of log p
-  uint16_t* g_out;          // [row_cap][g_ld] bf16, or nullptr (statistics mode)
+  uint16_t* g_out;          // [g_cols / 8][g_ld][8] bf16, or nullptr (statistics mode)
   int64_t g_ld, g_cols;
 };
 
 // Plain bf16 GEMM on the same 256 x 256 MFMA tile:
 //   C[s][m][n] (=|+=) sum_{k in split s} A(m, k) B(n, k)
-// Each operand is stored either K-contiguous (row m of A holds A(m, 0..K);
-// the "row" layout) or with K as its row (row k of A holds A(0..M, k); the
-// "K-row" layout, read with transposing LDS loads), so G, W and the hidden
-// rows are all used as stored.  K ranges are multiples of 64.
+// Each operand X (A indexed by m, B by n) is used as stored, in one of:
+//   kLayoutKRow    X(i, k) at k * ld + i (row k holds every i; W and hidden
+//                  rows for a contraction over the vocabulary or the rows);
+//   kLayoutCmRow   X(i, k) at ((k / 8) * ld + i) * 8 + k % 8 (chunk-major
+//                  along k: the logit gradient contracted over the vocabulary);
+//   kLayoutCmKRow  X(i, k) at ((i / 8) * ld + k) * 8 + i % 8 (chunk-major
+//                  along i: the logit gradient contracted over its rows).
+// K ranges are multiples of 64.
+constexpr int kLayoutKRow = 1, kLayoutCmRow = 2, kLayoutCmKRow = 3;
 struct GemmArgs {
   const void* a;
   int64_t lda;
-  int a_krow;               // layout of A: 0 row, 1 K-row
-  // K-row layout only: stored columns (multiple of 8; reads past them are
-  // clamped) and stored rows (reads of K rows past them are clamped; the
-  // other operand must hold zeros at those K).
+  int a_layout;
+  // K-row roles only: stored extent along i (a multiple of 8; reads past it
+  // are clamped) and stored K rows (reads of K rows past them are clamped;
+  // the other operand must hold zeros at those K).
   int64_t a_cols, a_krows;
   const void* b;
   int64_t ldb;
-  int b_krow;
+  int b_layout;
   int64_t b_cols, b_krows;
   int64_t m, n, k;          // sizes (upper bounds when a dimension is dynamic)
   // Dynamic dimension: dyn_dim 1 makes M = clamp(*dyn - dyn_base, 0, m);
@@ -99,7 +106,7 @@ hipError_t launch_compact(const uint8_t* mask, int64_t n_rows, int32_t* rows,
                           hipStream_t stream);
 hipError_t launch_lmhead(const LmheadArgs& a, int64_t grid, bool bf16, hipStream_t stream);
 hipError_t launch_lmhead_grad(const LmheadArgs& a, int64_t grid, hipStream_t stream);
-// Supported layouts (a_krow, b_krow): (0, 1) and (1, 1).
+// Supported layouts (a, b): (kLayoutCmRow, kLayoutKRow), (kLayoutCmKRow, kLayoutKRow).
 hipError_t launch_gemm(const GemmArgs& a, hipStream_t stream);
 // out[e][:] = e < n ? in[map[e]][:] : 0 for e < min(round_up(n, 64), cap), where
 // n = clamp(*dyn - dyn_base, 0, cap); out is [cap][d] bf16, d % 8 == 0.

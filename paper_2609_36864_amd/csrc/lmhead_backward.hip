@@ -47,35 +47,42 @@ __device__ __forceinline__ int krow_xor(int r) {
   return 2 * j1 + 4 * j0 + 8 * (j0 ^ j1);
 }
 
-// Per-lane DMA and fragment addressing of one operand of the tile.
-template <bool KROW>
-struct Operand {
-  uint32_t off[kBlocksPerWave];   // per-lane byte offset of each DMA block (row layout: final)
-  uint32_t colb[kBlocksPerWave];  // K-row layout: per-lane column byte offset of each DMA block
-  uint64_t tile;                  // uniform base of the tile
-  int64_t ld2;                    // bytes per stored row
-  int64_t krows;                  // K-row layout: stored rows
-  uint32_t frag[4];               // K-row layout: per-lane LDS byte offset of each 32-wide MFMA block
+// Chunk-major tiles in the K-row role: stored row r of the slice in chunk
+// c sits at slot c * 64 + (r ^ cm_xor(c)).  A transposing read by 32 lanes
+// touches 4 consecutive rows (64 bytes) in each of 4 consecutive chunks,
+// which start 1 KB apart (same bank): XOR-ing bits 2-3 of the row with the
+// chunk's two low bits puts the 4 segments in distinct 64-byte bank ranges
+// (and any 2 consecutive chunks in distinct 32-byte ranges of 128 bytes).
+__device__ __forceinline__ int cm_xor(int c) { return 4 * (c & 3); }
 
-  // row layout: the tile's rows t0 .. t0+255 (clamped to `rows`), K-contiguous.
-  // K-row layout: the tile's columns t0 .. t0+255 (clamped to `cols`) of every
-  // stored row.
-  __device__ __forceinline__ void init(const void* ptr, int64_t ld, int64_t t0, int64_t rows, int64_t cols,
+// Per-lane DMA and fragment addressing of one operand of the tile, by
+// stored layout (GemmArgs::a_layout / b_layout):
+//   kLayoutKRow   X(i, k) at k * ld + i: row k holds the tile's columns;
+//                 LDS slot of (row r, chunk c) = r * 32 + (c ^ krow_xor(r)).
+//   kLayoutCmRow  X(i, k) at ((k / 8) * ld + i) * 8 + k % 8 (chunk-major,
+//                 K split into chunks); LDS slot of (row i, chunk c) =
+//                 c * 256 + i, read with plain 16-byte loads.
+//   kLayoutCmKRow X(i, k) at ((i / 8) * ld + k) * 8 + i % 8 (chunk-major,
+//                 the tile's columns split into chunks); LDS slot as for
+//                 cm_xor above, read with transposing loads.
+// In every case one DMA block of 64 lanes fills 64 consecutive LDS slots,
+// and a K-slice fills 2048 slots (32 KB).
+template <int LAY>
+struct Operand {
+  uint32_t off[kBlocksPerWave];   // per-lane byte offset of each DMA block (kLayoutCmRow: final)
+  uint64_t tile;                  // uniform base of the tile
+  int64_t ld;                     // elements between stored rows (chunk-major: rows per chunk plane)
+  int64_t krows;                  // stored K rows (K-row roles)
+  uint32_t frag_lo[4], frag_hi[4];   // transposing reads: per-lane LDS byte offset of each 32-wide block
+
+  // t0: first column (tile index) of the tile; rows / cols: valid extent
+  // of that index (row role) or stored columns (K-row roles; a multiple of 8).
+  __device__ __forceinline__ void init(const void* ptr, int64_t ld_, int64_t t0, int64_t rows, int64_t cols,
                                        int64_t krows_, int wave, int lane, int nblk, int blk0) {
-    ld2 = ld * 2;
+    ld = ld_;
     krows = krows_;
-    if (!KROW) {
-      tile = reinterpret_cast<uint64_t>(ptr) + static_cast<uint64_t>(t0 * ld2);
-      const int lrow = lane / kChunks;
-#pragma unroll
-      for (int i = 0; i < kBlocksPerWave; ++i) {
-        const int r = wave * (kTileV / kWaves) + i * kBlockRows + lrow;
-        int64_t row = t0 + r;
-        row = row < rows ? row : rows - 1;
-        const int chunk = (lane % kChunks) ^ row_xor((wave * kBlocksPerWave + i) * kBlockRows + lrow);
-        off[i] = static_cast<uint32_t>((row - t0) * ld2 + chunk * 16);
-      }
-    } else {
+    const int a = lane & 15, gi = (lane >> 4) & 1, half = lane >> 5;
+    if (LAY == kLayoutKRow) {
       tile = reinterpret_cast<uint64_t>(ptr) + static_cast<uint64_t>(t0 * 2);
 #pragma unroll
       for (int i = 0; i < kBlocksPerWave; ++i) {
@@ -83,22 +90,50 @@ struct Operand {
         const int chunk = (lane & 31) ^ krow_xor(r);
         int64_t c = t0 + 8 * chunk;
         c = c < cols - 8 ? c : cols - 8;
-        colb[i] = static_cast<uint32_t>((c - t0) * 2);
+        off[i] = static_cast<uint32_t>((c - t0) * 2);   // + row * ld * 2 at issue
       }
-      // fragment reads: lane l of a 16-lane group reads stored row 4 j + l / 4
-      // (j: which half of the 8 K values) at columns 4 (l % 4) .. +3 of its
-      // group's 16 columns; lanes 32-63 take K values 8-15 of the sub-step
-      const int a = lane & 15, gi = (lane >> 4) & 1, half = lane >> 5;
+      // lane l of a 16-lane group reads stored row 4 j + l / 4 (j: which half
+      // of the 8 K values) at columns 4 (l % 4) .. +3 of its group's 16
+      // columns; lanes 32-63 take K values 8-15 of the sub-step
 #pragma unroll
       for (int bk = 0; bk < nblk; ++bk) {
         const int c = (((blk0 + bk * 32) >> 3) + 2 * gi + ((a & 3) >> 1)) ^ krow_xor(a >> 2);
-        frag[bk] = static_cast<uint32_t>(((a >> 2) + 8 * half) * (kKRowChunks * 16) + c * 16 + (a & 1) * 8);
+        frag_lo[bk] = static_cast<uint32_t>(((a >> 2) + 8 * half) * (kKRowChunks * 16) + c * 16 + (a & 1) * 8);
+        frag_hi[bk] = frag_lo[bk] + 4 * kKRowChunks * 16;
+      }
+    } else if (LAY == kLayoutCmRow) {
+      tile = reinterpret_cast<uint64_t>(ptr) + static_cast<uint64_t>(t0 * 16);
+#pragma unroll
+      for (int i = 0; i < kBlocksPerWave; ++i) {
+        // block wave*4 + i = slots (wave * 4 + i) * 64 ..: chunk `wave`, rows i * 64 + lane
+        int64_t row = t0 + i * 64 + lane;
+        row = row < rows ? row : rows - 1;
+        off[i] = static_cast<uint32_t>((wave * ld + (row - t0)) * 16);
+      }
+    } else {
+      const int64_t c0 = t0 / 8;
+      tile = reinterpret_cast<uint64_t>(ptr) + static_cast<uint64_t>(c0 * ld * 16);
+#pragma unroll
+      for (int i = 0; i < kBlocksPerWave; ++i) {
+        // block wave*4 + i = chunk c = wave * 4 + i, slot lane = row lane ^ cm_xor(c)
+        int64_t c = c0 + wave * kBlocksPerWave + i;
+        c = c < cols / 8 - 1 ? c : cols / 8 - 1;
+        off[i] = static_cast<uint32_t>((c - c0) * ld * 16);   // + row * 16 at issue
+      }
+#pragma unroll
+      for (int bk = 0; bk < nblk; ++bk) {
+        const int c = ((blk0 + bk * 32) >> 3) + 2 * gi + ((a & 3) >> 1);
+        const int r = 8 * half + (a >> 2);   // bits 2-3: 0 / half; + 4 j for the second read
+        frag_lo[bk] = static_cast<uint32_t>((c * 64 + (r ^ cm_xor(c))) * 16 + (a & 1) * 8);
+        frag_hi[bk] = static_cast<uint32_t>((c * 64 + ((r + 4) ^ cm_xor(c))) * 16 + (a & 1) * 8);
       }
     }
   }
-  // uniform address of K-slice starting at element k
+  // uniform address of the K-slice starting at element k
   __device__ __forceinline__ uint64_t slice_base(int64_t k) const {
-    return KROW ? tile + static_cast<uint64_t>(k * ld2) : tile + static_cast<uint64_t>(k * 2);
+    if (LAY == kLayoutKRow) return tile + static_cast<uint64_t>(k * ld * 2);
+    if (LAY == kLayoutCmRow) return tile + static_cast<uint64_t>((k / 8) * ld * 16);
+    return tile + static_cast<uint64_t>(k * 16);
   }
   // last stored row of the K-slice starting at element k, relative to it
   // (>= 0: every slice starts at a stored row; 63 when the slice is whole)
@@ -108,29 +143,35 @@ struct Operand {
   }
   // per-lane offset of DMA block i of a K-slice whose last stored row is rmax
   __device__ __forceinline__ uint32_t block_off(int i, int rmax, int wave, int lane) const {
-    if (!KROW) return off[i];
-    const int r = 2 * (wave * kBlocksPerWave + i) + (lane >> 5);
+    if (LAY == kLayoutCmRow) return off[i];
+    const int r = LAY == kLayoutKRow ? 2 * (wave * kBlocksPerWave + i) + (lane >> 5) : lane ^ (4 * i);
     const int rr = r < rmax ? r : rmax;
-    return static_cast<uint32_t>(rr) * static_cast<uint32_t>(ld2) + colb[i];
+    return LAY == kLayoutKRow ? static_cast<uint32_t>(rr) * static_cast<uint32_t>(ld * 2) + off[i]
+                              : static_cast<uint32_t>(rr) * 16u + off[i];
+  }
+  // the 16-byte MFMA fragment of 32-wide block bk (first column mbase of the
+  // tile) for sub-step kk: 8 consecutive K values of column mbase + lane % 32
+  __device__ __forceinline__ uint4 frag(const uint4* stage_op, int bk, int mbase, int kk, int lane) const {
+    if (LAY == kLayoutCmRow) return stage_op[(kk * 2 + (lane >> 5)) * kTileV + mbase + (lane & 31)];
+    typedef __attribute__((address_space(3))) i16x4_t lds_i16x4;
+    const char __attribute__((address_space(3)))* base =
+        (const char __attribute__((address_space(3)))*)(
+            (const __attribute__((address_space(3))) uint4*)stage_op);
+    // sub-step kk covers stored rows 16 kk .. 16 kk + 15 (untouched by the XOR patterns)
+    const uint32_t ks = static_cast<uint32_t>(kk * 16 * (LAY == kLayoutKRow ? kKRowChunks * 16 : 16));
+    const i16x4_t lo = __builtin_amdgcn_ds_read_tr16_b64_v4i16((lds_i16x4*)(base + frag_lo[bk] + ks));
+    const i16x4_t hi = __builtin_amdgcn_ds_read_tr16_b64_v4i16((lds_i16x4*)(base + frag_hi[bk] + ks));
+    const uint2 l = __builtin_bit_cast(uint2, lo), h = __builtin_bit_cast(uint2, hi);
+    return make_uint4(l.x, l.y, h.x, h.y);
   }
 };
-
-// 16 bytes of an MFMA fragment (8 consecutive K values of one column) from a
-// K-row LDS tile: two transposing 8-byte reads, 4 K values each.
-__device__ __forceinline__ uint4 krow_frag(const char __attribute__((address_space(3)))* base, uint32_t off) {
-  typedef __attribute__((address_space(3))) i16x4_t lds_i16x4;
-  const i16x4_t lo = __builtin_amdgcn_ds_read_tr16_b64_v4i16((lds_i16x4*)(base + off));
-  const i16x4_t hi = __builtin_amdgcn_ds_read_tr16_b64_v4i16((lds_i16x4*)(base + off + 4 * kKRowChunks * 16));
-  const uint2 l = __builtin_bit_cast(uint2, lo), h = __builtin_bit_cast(uint2, hi);
-  return make_uint4(l.x, l.y, h.x, h.y);
-}
 
 // C[s][m][n] (=|+=) sum_k A(m, k) B(n, k) over the K range of split s, for
 // one 256 x 256 tile of C per workgroup.  Same data path as the fused
 // kernel: K-slices of 64 K values stream into a 2-stage LDS ring by direct
 // DMA; eight waves each own 128 x 64 of the tile as 4 x 2 MFMA blocks.
-// AK / BK: operand stored with K as its row.
-template <bool AK, bool BK>
+// LA / LB: stored layouts of A and B (see Operand).
+template <int LA, int LB>
 __global__ __launch_bounds__(kThreads, 1) void gemm_kernel(GemmArgs p) {
   using M = Mma<true>;
   static_assert(kWaves == 8 && kNB == 2, "8-wave tile layout assumed");
@@ -185,14 +226,12 @@ __global__ __launch_bounds__(kThreads, 1) void gemm_kernel(GemmArgs p) {
       for (int q = 0; q < 16; ++q) acc[bm][bn][q] = 0.f;
 
   if (n_iter > 0) {
-    Operand<AK> A;
-    Operand<BK> B;
+    Operand<LA> A;
+    Operand<LB> B;
     A.init(p.a, p.lda, tm * kTileV, m_valid, p.a_cols, p.a_krows, wave, lane, 4, wm * 128);
     B.init(p.b, p.ldb, tn * kTileN, p.n, p.b_cols, p.b_krows, wave, lane, kNB, wn * kWaveN);
     const uint32_t lds_base = static_cast<uint32_t>(
         reinterpret_cast<size_t>((__attribute__((address_space(3))) uint4*)(&lds[0][0][0])));
-    const char __attribute__((address_space(3)))* lds_bytes =
-        (const char __attribute__((address_space(3)))*)(&lds[0][0][0]);
     auto lds_addr = [&](int stage, int op, int block) -> uint32_t {
       return __builtin_amdgcn_readfirstlane(
           lds_base + static_cast<uint32_t>(((stage * 2 + op) * kSlots + block * 64) * 16));
@@ -204,8 +243,8 @@ __global__ __launch_bounds__(kThreads, 1) void gemm_kernel(GemmArgs p) {
       const int64_t k = k0 + static_cast<int64_t>(slice) * kGemmSliceK;
       a_slice = A.slice_base(k);
       b_slice = B.slice_base(k);
-      if (AK) a_rmax = A.slice_rmax(k);
-      if (BK) b_rmax = B.slice_rmax(k);
+      if (LA != kLayoutCmRow) a_rmax = A.slice_rmax(k);
+      if (LB != kLayoutCmRow) b_rmax = B.slice_rmax(k);
     };
     auto issue_one = [&](int jj) {
       const int i = jj % kBlocksPerWave;
@@ -216,18 +255,10 @@ __global__ __launch_bounds__(kThreads, 1) void gemm_kernel(GemmArgs p) {
     };
     auto load_frags = [&](int slice, int kk, uint4 (&fa)[4], uint4 (&fb)[kNB]) {
       const int stage = slice % kStages;
-      // K-row tiles: sub-step kk covers stored rows 16 kk .. 16 kk + 15
-      const uint32_t ks = static_cast<uint32_t>(kk * 16 * kKRowChunks * 16);
 #pragma unroll
-      for (int bm = 0; bm < 4; ++bm) {
-        if (AK) fa[bm] = krow_frag(lds_bytes + (stage * 2 + 0) * kSlots * 16, A.frag[bm] + ks);
-        else fa[bm] = lds[stage][0][swz(wm * 128 + bm * 32 + col, kk * 2 + half)];
-      }
+      for (int bm = 0; bm < 4; ++bm) fa[bm] = A.frag(lds[stage][0], bm, wm * 128 + bm * 32, kk, lane);
 #pragma unroll
-      for (int bn = 0; bn < kNB; ++bn) {
-        if (BK) fb[bn] = krow_frag(lds_bytes + (stage * 2 + 1) * kSlots * 16, B.frag[bn] + ks);
-        else fb[bn] = lds[stage][1][swz(wn * kWaveN + bn * 32 + col, kk * 2 + half)];
-      }
+      for (int bn = 0; bn < kNB; ++bn) fb[bn] = B.frag(lds[stage][1], bn, wn * kWaveN + bn * 32, kk, lane);
     };
 
     const int n_pre = n_iter < kStages ? n_iter : kStages;
@@ -346,10 +377,10 @@ hipError_t launch_gemm(const GemmArgs& a, hipStream_t stream) {
   const int64_t grid = (groups + kNumXcd - 1) / kNumXcd * kNumXcd * per_group;
   if (grid <= 0) return hipSuccess;
   const dim3 g(static_cast<unsigned>(grid)), blk(kThreads);
-  if (!a.a_krow && a.b_krow)
-    hipLaunchKernelGGL((gemm_kernel<false, true>), g, blk, 0, stream, a);
-  else if (a.a_krow && a.b_krow)
-    hipLaunchKernelGGL((gemm_kernel<true, true>), g, blk, 0, stream, a);
+  if (a.a_layout == kLayoutCmRow && a.b_layout == kLayoutKRow)
+    hipLaunchKernelGGL((gemm_kernel<kLayoutCmRow, kLayoutKRow>), g, blk, 0, stream, a);
+  else if (a.a_layout == kLayoutCmKRow && a.b_layout == kLayoutKRow)
+    hipLaunchKernelGGL((gemm_kernel<kLayoutCmKRow, kLayoutKRow>), g, blk, 0, stream, a);
   else
     return hipErrorInvalidValue;
   return hipGetLastError();

@@ -85,9 +85,10 @@ __device__ __forceinline__ void combine(float& m, float& s, float& z, float& t, 
 //                baseline);
 //   kEpiGrad:    the gradient of log p with respect to the logits,
 //                g (1[v == y] - exp(z - lse)), written as bf16 (backward pass;
-//                lse comes from the forward pass), with zero rows up to the
-//                next multiple of 64 rows so that a contraction over rows
-//                can run in whole 64-row K-slices.
+//                lse comes from the forward pass), chunk-major (8 vocabulary
+//                entries of a row, then the same 8 of the next row), with
+//                zero rows up to the next multiple of 64 rows so that a
+//                contraction over rows can run in whole 64-row K-slices.
 constexpr int kEpiStats = 0, kEpiEntropy = 1, kEpiGrad = 2;
 
 template <bool BF16, bool KTAIL, int EPI>
@@ -336,50 +337,53 @@ __global__ __launch_bounds__(kThreads, 1) void lmhead_logprob_kernel(LmheadArgs 
   };
 
   // Gradient mode: G = g (1[v == y] - p) for the 4 x kNB blocks of this wave,
-  // rounded to bf16.  A lane holds 4-row runs 8 rows apart; lanes l and
-  // l + 32 exchange half of their runs so that each ends with 16 consecutive
-  // vocabulary entries of its token row (32 bytes, two 16-byte stores).
-  // Rows >= V hold -inf, so p = 0 and G = 0 there, which zero-fills the
-  // columns up to g_cols.
+  // rounded to bf16.  A lane holds runs of 4 consecutive vocabulary entries
+  // of its token row, 8 entries apart; lanes l and l + 32 hold the two
+  // halves of each 8-entry chunk.  G is stored chunk-major, so one 8-byte
+  // store per run covers 512 contiguous bytes across the wave (32 token
+  // rows x one chunk).  Rows >= V hold -inf, so p = 0 and G = 0 there, which
+  // zero-fills the columns up to g_cols.
   auto grad_epilogue = [&](int64_t vt) {
-    const int64_t vbase = vt * kTileV + wm * 128;
+    const int vbase = static_cast<int>(vt * kTileV) + wm * 128;   // V < 2^31
 #pragma unroll
     for (int bn = 0; bn < kNB; ++bn) {
       const int64_t e = rt * kTileN + wn * kWaveN + bn * 32 + col;
       const bool live = e < n_s;   // rows n_s .. round_up(n_s, 64) - 1 are written as zeros
-      uint16_t* grow = p.g_out + e * p.g_ld;
+      uint16_t* gcol = p.g_out + e * 8;   // chunk c of this row: gcol + c * g_ld * 8
+      const float gneg = -g_up[bn];
 #pragma unroll
       for (int bm = 0; bm < 4; ++bm) {
+        // element q of this lane's block is column v0 + 8 (q / 4) + q % 4
+        const int v0 = vbase + bm * 32 + 4 * half;
+        float gv[16];
+#pragma unroll
+        for (int q = 0; q < 16; ++q)
+          gv[q] = gneg * fast_exp2(__builtin_fmaf(acc[bm][bn][q], kLog2e, -g_lse[bn]));
+        // The sampled token's column gets g (1 - p) instead: at most one
+        // element per row, so the branch is rarely taken by any lane.
+        const int dt = tok[bn] - v0;
+        if (static_cast<unsigned>(dt) < 28u && (dt & 4) == 0) {
+          const int qi = (dt >> 3) * 4 + (dt & 3);
+#pragma unroll
+          for (int q = 0; q < 16; ++q)
+            if (q == qi) gv[q] = g_up[bn] * (1.f - fast_exp2(__builtin_fmaf(acc[bm][bn][q], kLog2e, -g_lse[bn])));
+        }
         uint32_t pk[4][2];   // [run jr][pair]: rows 8 jr + 4 half + {0,1 | 2,3}
 #pragma unroll
         for (int jr = 0; jr < 4; ++jr)
 #pragma unroll
           for (int r = 0; r < 4; r += 2) {
-            const int64_t v = vbase + bm * 32 + 8 * jr + 4 * half + r;
-            float gv[2];
-#pragma unroll
-            for (int u = 0; u < 2; ++u) {
-              const float pv = fast_exp2(__builtin_fmaf(acc[bm][bn][jr * 4 + r + u], kLog2e, -g_lse[bn]));
-              gv[u] = !live ? 0.f : (v + u == tok[bn]) ? g_up[bn] * (1.f - pv) : -g_up[bn] * pv;
-            }
-            pk[jr][r / 2] = static_cast<uint32_t>(__builtin_bit_cast(uint16_t, static_cast<__bf16>(gv[0]))) |
-                            (static_cast<uint32_t>(__builtin_bit_cast(uint16_t, static_cast<__bf16>(gv[1]))) << 16);
+            const uint32_t w = static_cast<uint32_t>(__builtin_bit_cast(uint16_t, static_cast<__bf16>(gv[jr * 4 + r]))) |
+                               (static_cast<uint32_t>(__builtin_bit_cast(uint16_t, static_cast<__bf16>(gv[jr * 4 + r + 1])))
+                                << 16);
+            pk[jr][r / 2] = live ? w : 0u;
           }
-        // lane half 0 keeps runs 0, 1 and takes its partner's; half 1 keeps 2, 3
-        uint32_t rv[4];
+        // run jr of this lane = entries v0 + 8 jr .. +3 = bytes 8 half .. +7 of chunk (v0 / 8 + jr)
+        if (e < n_s_pad && vbase + bm * 32 < p.g_cols) {
+          uint16_t* dst = gcol + ((vbase + bm * 32) / 8) * p.g_ld * 8 + 4 * half;
 #pragma unroll
-        for (int q = 0; q < 4; ++q) {
-          const uint32_t send = half == 0 ? pk[2 + q / 2][q % 2] : pk[q / 2][q % 2];
-          rv[q] = static_cast<uint32_t>(__shfl_xor(static_cast<int>(send), 32));
-        }
-        const uint4 lo = half == 0 ? make_uint4(pk[0][0], pk[0][1], rv[0], rv[1])
-                                   : make_uint4(rv[0], rv[1], pk[2][0], pk[2][1]);
-        const uint4 hi = half == 0 ? make_uint4(pk[1][0], pk[1][1], rv[2], rv[3])
-                                   : make_uint4(rv[2], rv[3], pk[3][0], pk[3][1]);
-        const int64_t v16 = vbase + bm * 32 + 16 * half;   // first of this lane's 16 entries
-        if (e < n_s_pad && v16 < p.g_cols) {
-          *reinterpret_cast<uint4*>(grow + v16) = lo;
-          *reinterpret_cast<uint4*>(grow + v16 + 8) = hi;
+          for (int jr = 0; jr < 4; ++jr)
+            *reinterpret_cast<uint2*>(dst + jr * p.g_ld * 8) = make_uint2(pk[jr][0], pk[jr][1]);
         }
       }
     }

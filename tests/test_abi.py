@@ -103,7 +103,9 @@ def test_backward_workspace_and_argument_errors(lib):
     n, d, V = 1000, 64, 1000
     size = ws(n, d, V, 1)
     assert size >= 2 * 1024 * 1024 + 2 * 1024 * d and size < 2 * 1024 * 1024 + 40 * 1024 * d
-    assert ws(n, d, (1 << 23) - 64, 1) > 0 and ws(n, d, (1 << 23) - 63, 1) == 0   # vocabulary limit
+    assert ws(n, d, 1 << 23, 1) > 0 and ws(n, d, (1 << 30) + 1, 1) == 0   # vocabulary limit
+    # G is held for one chunk of at most 32768 rows: more rows only lengthen the row list
+    assert 0 < ws(100000, d, V, 1) - ws(32768, d, V, 1) < 4 * 100000
     assert ws(n, (1 << 23) + 8, V, 1) == 0
     assert ws(n, d, V, 0) == 0          # fp32 inputs are not supported
     assert ws(n, 12, V, 1) == 0         # d not a multiple of 8

@@ -68,10 +68,10 @@ def test_backward_matches_oracle(hdl, n, d, V):
 
 
 def test_backward_several_chunks(hdl):
-    # more than 8192 scored rows: G is produced in two chunks and dW summed over them
-    H, W, y, m, up = _case(17000, 64, 512, seed=31, mask_p=0.6)
+    # more than 2 x 32768 scored rows: G is produced in three chunks and dW summed over them
+    H, W, y, m, up = _case(80000, 64, 512, seed=31, mask_p=0.9)
     dh, dw = _gpu(hdl, H, W, y, m, up)
-    assert int(m.sum()) > 8192
+    assert int(m.sum()) > 2 * 32768
     want_dh, want_dw, mag_dh, mag_dw = O.token_logprobs_backward(as_f64(H), as_f64(W), y.numpy(),
                                                                  up.double().numpy(), m.numpy())
     _check(dh, want_dh, mag_dh, "dH")
