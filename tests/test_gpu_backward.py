@@ -56,6 +56,9 @@ def _check(got, want, mag, what):
     (257, 72, 4133),     # K tail in the logit recompute, ragged GEMM edges
     (40, 8, 300),        # d smaller than one K-slice
     (700, 256, 20000),   # realistic vocabulary tail, several vocabulary splits
+    (1, 16, 65),         # one row; one vocabulary entry past a 64-multiple
+    (33, 200, 129),      # d not a multiple of 64 (K tail; clamped W columns in dH)
+    (600, 64, 257),      # a last vocabulary tile with one live column; ragged scored-row count
 ])
 def test_backward_matches_oracle(hdl, n, d, V):
     H, W, y, m, up = _case(n, d, V, seed=n + d + V)
