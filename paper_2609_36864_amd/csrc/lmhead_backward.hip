@@ -7,18 +7,19 @@
 //     dL/dh_n = sum_v G[n][v] W[v]        (dH = G W)
 //     dL/dW_v = sum_n G[n][v] h_n         (dW = G^T H)
 //
-// G is produced chunk by chunk (at most a few thousand rows at a time, so the
-// rows x vocabulary tensor never exists whole) by the fused lm-head kernel in
-// its gradient mode, which recomputes the logits tile by tile.  The two
+// G is produced chunk by chunk (at most 32,768 rows at a time, so the rows x
+// vocabulary tensor is bounded) by the fused lm-head kernel in its gradient
+// mode, which recomputes the logits tile by tile and stores G chunk-major
+// (8 vocabulary entries of a row, then the same 8 of the next row).  The two
 // contractions are plain bf16 GEMMs on the same 256 x 256 MFMA tile as the
-// forward kernel (gemm_kernel below).  Each operand is read as stored: G is
-// K-contiguous for dH and has the contracted index as its row for dW, W and
-// the chunk's hidden rows (gathered into a dense block by gather_rows_kernel)
-// have it as their row; those operands are staged in LDS as stored and turned
-// into MFMA fragments by gfx950's transposing LDS reads, so nothing is
-// transposed in memory.  dH is split along the vocabulary for parallelism and
-// its partial sums are added in a fixed order (splitk_scatter_kernel): the
-// whole pass is deterministic.
+// forward kernel (gemm_kernel below), each operand read as stored: G in
+// either role, W, and the chunk's hidden rows (gathered into a dense block by
+// gather_rows_kernel).  Operands whose stored rows run along the contracted
+// index are staged in LDS as stored and turned into MFMA fragments by
+// gfx950's transposing LDS reads, so nothing is transposed in memory.  dH is
+// split along the vocabulary when it has too few tiles for the chip, and its
+// partial sums are added in a fixed order (splitk_scatter_kernel): the whole
+// pass is deterministic.
 #include "tile_common.h"
 
 namespace hdl {
@@ -28,7 +29,7 @@ using namespace tile;
 
 constexpr int kGemmSliceK = 8 * kChunks;   // bf16 elements per K-slice
 // K-row operand tiles: a K-slice is 64 stored rows of kTileV bf16 (512 bytes,
-// 32 chunks of 16 bytes), the same 32 KB as a row-layout slice.
+// 32 chunks of 16 bytes), 32 KB like every operand stage.
 constexpr int kKRowChunks = kTileV * 2 / 16;
 static_assert(kGemmSliceK * kKRowChunks == kSlots, "K-row slice must fill one operand stage");
 static_assert(2 * kKRowChunks == 64, "one DMA block must hold two stored K rows");

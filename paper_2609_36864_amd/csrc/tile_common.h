@@ -1,5 +1,5 @@
 // Building blocks shared by the MFMA tile kernels of libhdl.so (the fused
-// lm-head kernel and the plain NT GEMM of the backward pass): the 256 x 256
+// lm-head kernel and the plain GEMM of the backward pass): the 256 x 256
 // workgroup tile, its LDS ring of K-slices with XOR-swizzled 16-byte chunks,
 // the direct global -> LDS DMA, explicit memory-counter waits, and the MFMA
 // step for bf16 and fp32 operands.  Not part of the public ABI.
