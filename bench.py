@@ -76,7 +76,7 @@ def mfma_ceiling():
     return json.loads(r.stdout.strip().splitlines()[-1])
 
 
-def cpu_baseline(w, budget_s: float = 15.0, max_rows: int = 4096, entropy: bool = False):
+def cpu_baseline(w, budget_s: float = 15.0, max_rows: int = 32768, entropy: bool = False):
     """Time the float64 oracle on a seeded sample of eligible rows (both
     contexts; the original context only for the entropy selector) on the host
     cores; return oracle scored tokens/s."""
