@@ -62,6 +62,35 @@ def measured_traffic(workload: str):
     return rec.get("hbm_bytes_per_launch")
 
 
+def library_gemm_tflops(h, W, rows: int = 16384, reps: int = 3):
+    """Reference point, not part of the path: the vendor library's plain bf16
+    GEMM (torch.matmul -> hipBLASLt) on the same contraction, logits = h W^T
+    for the scored rows, written as bf16 in row chunks into one reused
+    buffer.  The fused kernel does this contraction plus the online
+    log-sum-exp and never writes the logits."""
+    import torch
+    n = h.shape[0]
+    out = torch.empty(min(rows, n), W.shape[0], dtype=torch.bfloat16, device=h.device)
+
+    def run():
+        for r0 in range(0, n, rows):
+            r1 = min(n, r0 + rows)
+            torch.matmul(h[r0:r1], W.t(), out=out[: r1 - r0])
+
+    run()
+    torch.cuda.synchronize()
+    e0 = torch.cuda.Event(enable_timing=True)
+    e1 = torch.cuda.Event(enable_timing=True)
+    e0.record()
+    for _ in range(reps):
+        run()
+    e1.record()
+    torch.cuda.synchronize()
+    ms = e0.elapsed_time(e1) / reps
+    del out
+    return 2.0 * n * h.shape[1] * W.shape[0] / (ms / 1e3) / 1e12
+
+
 def mfma_ceiling():
     """Run the built MFMA ceiling microbenchmark (paper_2609_36864_amd/mfma_ceiling)
     in a child process; returns its JSON record or None if it is not built."""
@@ -138,7 +167,8 @@ def main() -> int:
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--cpu-budget", type=float, default=15.0)
     ap.add_argument("--no-mfma-ceiling", action="store_true",
-                    help="skip measuring this GPU's MFMA ceilings (const/random operands)")
+                    help="skip measuring this GPU's MFMA ceilings (const/random operands) and the "
+                         "library GEMM reference")
     ap.add_argument("--copy-probe-mb", type=int, default=0,
                     help="after timing, copy this many MiB device-to-device once (a known-size "
                          "kernel that calibrates rocprofv3 FETCH_SIZE / WRITE_SIZE)")
@@ -288,6 +318,12 @@ def main() -> int:
             ceil["frac_of_random_operand_ceiling"] = achieved / ceil["random_operands_tflops"]
             result["roofline"]["measured_ceiling"] = ceil
             log(f"MFMA ceilings: {ceil}")
+        lib = library_gemm_tflops(hidden[mask.bool()], W)
+        result["roofline"]["library_gemm"] = {
+            "what": "torch.matmul(scored hidden rows, W^T) -> bf16 logits (hipBLASLt), same contraction, "
+                    "16384-row chunks; reference only",
+            "tflops": lib, "fused_kernel_frac": achieved / lib}
+        log(f"library GEMM on the same contraction: {lib:.0f} TFLOP/s (fused kernel: {achieved / lib:.3f} of it)")
     traffic = None if ent_sel else measured_traffic(args.workload)
     if traffic is not None:
         result["roofline"]["traffic"] = traffic
