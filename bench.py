@@ -457,6 +457,34 @@ def bench_backward(args, w, hdl, dev) -> int:
                      "whole_pass": {"ms": step_ms, "flops": flops, "achieved": achieved,
                                     "frac": achieved / peak}},
     }
+    if not args.no_mfma_ceiling:
+        # reference only: the vendor GEMMs (torch.matmul -> hipBLASLt) on the
+        # two contractions' shapes, with a bf16 logit gradient of the same size
+        gref = torch.randn(n_scored, c.V, device=dev, dtype=torch.bfloat16)
+        hs = hidden[mask.bool()]
+        dh_ref = torch.empty(n_scored, c.d, device=dev, dtype=torch.bfloat16)
+        dw_ref = torch.empty(c.V, c.d, device=dev, dtype=torch.bfloat16)
+        ref = {}
+        for name, fn in (("dH = G W", lambda: torch.matmul(gref, W, out=dh_ref)),
+                         ("dW = G^T H", lambda: torch.matmul(gref.t(), hs, out=dw_ref))):
+            fn()
+            torch.cuda.synchronize()
+            e0 = torch.cuda.Event(enable_timing=True)
+            e1 = torch.cuda.Event(enable_timing=True)
+            e0.record()
+            for _ in range(3):
+                fn()
+            e1.record()
+            torch.cuda.synchronize()
+            ref[name] = 2.0 * n_scored * c.V * c.d / (e0.elapsed_time(e1) / 3 / 1e3) / 1e12
+        del gref, dh_ref, dw_ref
+        result["roofline"]["library_gemm"] = {
+            "what": "torch.matmul (hipBLASLt) on the dH and dW shapes with a bf16 logit gradient, "
+                    "bf16 outputs; reference only",
+            "tflops": ref,
+            # both GEMMs have the same flops: their combined rate is the harmonic mean
+            "gemm_kernel_frac": gemm_tflops / (len(ref) / sum(1.0 / r for r in ref.values()))}
+        log(f"library GEMMs on the same shapes: {ref}")
     if not args.no_cpu_baseline:
         log("timing the float64 oracle backward on a bounded sample")
         result["cpu_baseline"] = cpu_baseline_backward(w, budget_s=args.cpu_budget)
