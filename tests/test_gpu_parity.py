@@ -308,6 +308,70 @@ def test_hidden_states_over_4gib_split_into_launches(hdl):
                                     torch.zeros(n, device="cuda"))
 
 
+def test_weight_over_4gib(hdl):
+    # W of 262,400 x 8192 bf16 (4.3 GB): the DMA addresses W through a 64-bit
+    # base per vocabulary tile and 32-bit offsets inside it.  W is zero except
+    # a few random rows (the last row before the 4 GiB offset and three past
+    # it among them), so every other
+    # logit is exactly 0 and the log-sum-exp has a closed form:
+    #     lse = log(sum_special exp(z_v) + (V - #special) * exp(0)).
+    # The backward pass is checked the same way: dL/dh only sees the special
+    # rows, and every zero row of W that is nobody's token gets the same
+    # dL/dW = -sum_n g_n exp(-lse_n) h_n.
+    d, V, n = 8192, 262400, 96
+    assert V * d * 2 > 2 ** 32
+    dev = "cuda"
+    gen = torch.Generator().manual_seed(404)
+    special = np.array([0, 1000, 131071, 262143, 262144, 262300, V - 1])
+    assert np.sum(special * d * 2 >= 2 ** 32) == 3 and (262143 + 1) * d * 2 == 2 ** 32
+    Ws = (torch.randn(len(special), d, generator=gen) * 0.05).to(torch.bfloat16)
+    W = torch.zeros(V, d, dtype=torch.bfloat16, device=dev)
+    W[torch.as_tensor(special, device=dev)] = Ws.to(dev)
+    H = torch.randn(n, d, generator=gen).to(torch.bfloat16)
+    rng = np.random.default_rng(404)
+    y = special[rng.integers(0, len(special), n)]
+    y[::7] = 262200                     # a zero row past 4 GiB as the sampled token
+    y[3::11] = 5                        # and one before it
+    y = y.astype(np.int32)
+    Hd, yd = H.to(dev), torch.from_numpy(y).to(dev)
+    lp, lse = hdl.token_logprobs(Hd, W, yd, None)
+    torch.cuda.synchronize()
+    z = as_f64(H) @ as_f64(Ws).T                          # [n, #special], exact products of the inputs
+    m = np.maximum(z.max(axis=1), 0.0)
+    want_lse = m + np.log(np.exp(z - m[:, None]).sum(axis=1) + (V - len(special)) * np.exp(-m))
+    col = {int(v): j for j, v in enumerate(special)}
+    z_y = np.array([z[i, col[int(t)]] if int(t) in col else 0.0 for i, t in enumerate(y)])
+    assert np.abs(lp.cpu().numpy() - (z_y - want_lse)).max() <= TOL_BF16
+    assert np.abs(lse.cpu().numpy() - want_lse).max() <= TOL_BF16
+
+    up = torch.from_numpy(rng.normal(size=n).astype(np.float32))
+    dh, dw = hdl.token_logprobs_backward(Hd, W, yd, None, lse, up.to(dev))
+    torch.cuda.synchronize()
+    g = up.double().numpy()
+    p = np.exp(z - want_lse[:, None])                     # probabilities of the special rows
+    G = -g[:, None] * p
+    for i, t in enumerate(y):
+        if int(t) in col:
+            G[i, col[int(t)]] += g[i]
+    want_dh = G @ as_f64(Ws)
+    mag_dh = np.abs(G) @ np.abs(as_f64(Ws))
+    got_dh = dh.cpu().double().numpy()
+    assert np.all(np.abs(got_dh - want_dh) <= 2.0 ** -8 * mag_dh + 1e-6 * mag_dh.max())
+    H64 = as_f64(H)
+    p0 = np.exp(-want_lse)                                # probability of every zero row
+    checks = {int(v): G[:, j] for j, v in enumerate(special)}
+    checks[262350] = -g * p0                              # nobody's token, past 4 GiB
+    checks[77] = -g * p0                                  # nobody's token, before it
+    for t in (262200, 5):
+        checks[t] = g * ((y == t).astype(np.float64) - p0)
+    rows = np.array(sorted(checks))
+    got_dw = dw[torch.as_tensor(rows, device=dev)].cpu().double().numpy()
+    for r, got in zip(rows, got_dw):
+        want = checks[int(r)] @ H64
+        mag = np.abs(checks[int(r)]) @ np.abs(H64)
+        assert np.all(np.abs(got - want) <= 2.0 ** -8 * mag + 1e-6 * mag.max()), f"dW row {r}"
+
+
 def test_non_finite_hidden_row_stays_local(hdl):
     # a NaN or Inf in one row's hidden state makes that row's log p NaN (its
     # logits are NaN); every other row of the same tile is unaffected, and
