@@ -17,7 +17,8 @@
 //
 // Work item: 256 vocabulary rows x 256 token rows per V-tile, looping over
 // the V-tiles of one chunk.  Eight waves per workgroup (two per SIMD, so one
-// wave's memory and epilogue work overlaps the other's MFMAs), each owning
+// wave's LDS reads and DMA issue overlap the other's MFMAs; the per-V-tile
+// epilogue, which both reach after the same slice, does not), each owning
 // 128 vocab x 64 tokens as a 4x2 grid of 32x32 MFMA blocks with fp32
 // accumulators.
 // W is the MFMA "A" operand (vocabulary on the M axis) and the hidden states
