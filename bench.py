@@ -40,17 +40,30 @@ def log(msg: str) -> None:
     print(f"[bench] {msg}", file=sys.stderr, flush=True)
 
 
+# Sources the fused kernel is compiled from.
+KERNEL_SOURCES = ("lmhead_logprob.hip", "tile_common.h", "hdl_internal.h")
+
+
 def kernel_source_sha() -> str:
+    """SHA-256 of the fused kernel's sources with comments and blank lines
+    removed, so that a comment edit does not invalidate counters taken on
+    the same code."""
     import hashlib
-    path = os.path.join(ROOT, "paper_2609_36864_amd", "csrc", "lmhead_logprob.hip")
-    with open(path, "rb") as f:
-        return hashlib.sha256(f.read()).hexdigest()
+    import re
+    h = hashlib.sha256()
+    for name in KERNEL_SOURCES:
+        with open(os.path.join(ROOT, "paper_2609_36864_amd", "csrc", name)) as f:
+            text = f.read()
+        text = re.sub(r"/\*.*?\*/", "", text, flags=re.S)
+        text = re.sub(r"//[^\n]*", "", text)
+        h.update("\n".join(line.rstrip() for line in text.splitlines() if line.strip()).encode())
+    return h.hexdigest()
 
 
 def measured_traffic(workload: str):
     """HBM bytes per launch of the fused kernel, from the committed rocprofv3
     FETCH_SIZE / WRITE_SIZE summary, if it was taken on the current kernel
-    source; otherwise None."""
+    sources (kernel_source_sha); otherwise None."""
     path = os.path.join(ROOT, "profiles", f"lmhead_logprob_{workload}_traffic.json")
     try:
         with open(path) as f:
