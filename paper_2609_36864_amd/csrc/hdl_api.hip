@@ -93,10 +93,11 @@ LmheadPlan make_plan(int64_t n_rows_total, int64_t vocab, int64_t d, int esz) {
   p.n_rows = n_rows;
   p.n_vt = (vocab + kTileV - 1) / kTileV;
   p.n_rt_max = (n_rows + kTileN - 1) / kTileN;
-  // Vocabulary tiles per work item: long items amortise the per-item merge
-  // and partial write; short ones balance the tail across 256 CUs.  Aim for
-  // at least ~2048 items when the problem allows.
-  int64_t tpc = (p.n_rt_max * p.n_vt) / 2048;
+  // Vocabulary tiles per work item: long items amortise the per-item
+  // pipeline fill and partial write; short ones balance the tail across 256
+  // CUs.  Aim for about 32 items per CU (measured: at 16,384 rows this runs
+  // 6 % faster than 8 items per CU; at 65,536 rows both give 16 tiles).
+  int64_t tpc = (p.n_rt_max * p.n_vt) / 8192;
   if (tpc < 1) tpc = 1;
   if (tpc > 16) tpc = 16;
   p.tpc = tpc;
