@@ -1,0 +1,91 @@
+"""Invariants of the LDS layouts the backward GEMM reads with gfx950's
+transposing loads (ds_read_b64_tr_b16), checked on the CPU by enumeration.
+
+The read's lane mapping, as measured on the GPU: within each group of 16
+lanes, lane i receives element i mod 4 of the 8-byte pieces addressed by
+lanes i/4, i/4 + 4, i/4 + 8 and i/4 + 12 of its group.
+
+Layouts (16-byte slots; a K-slice holds 64 stored rows of 256 columns):
+  K-row:        slot(row r, chunk c) = 32 r + (c ^ krow_xor(r))
+  chunk-major:  slot(row r, chunk c) = 64 c + (r ^ cm_xor(c))
+For each, a lane reading block columns m0 .. m0+31 at sub-step kk addresses
+row 16 kk + 8 half + 4 j + a/4 and column m0 + 16 g + 4 (a mod 4) (a = lane
+mod 16, g = (lane / 16) mod 2, half = lane / 32, j = which 4 of its 8 K
+values).  Checked: the result is the MFMA operand (column m0 + lane mod 32,
+K values 8 half .. 8 half + 7 of the sub-step, in order), and the 16- and
+32-lane subsets a transposing read serves together land in distinct bank
+ranges whether the LDS serves 128 or 256 bytes per clock.
+"""
+
+
+def krow_xor(r):
+    j0, j1 = r & 1, (r >> 1) & 1
+    return 2 * j1 + 4 * j0 + 8 * (j0 ^ j1)
+
+
+def cm_xor(c):
+    return 4 * (c & 3)
+
+
+def slot_krow(r, c):
+    return 32 * r + (c ^ krow_xor(r))
+
+
+def slot_cm(r, c):
+    return 64 * c + (r ^ cm_xor(c))
+
+
+def lane_address(slot_fn, lane, kk, j, m0):
+    a, g, half = lane & 15, (lane >> 4) & 1, lane >> 5
+    r = 16 * kk + 8 * half + 4 * j + a // 4
+    m = m0 + 16 * g + 4 * (a % 4)
+    return slot_fn(r, m // 8) * 16 + (m % 8) * 2, (r, m)
+
+
+def transposed_read(slot_fn, kk, j, m0):
+    """Emulate one ds_read_b64_tr_b16: per lane, the 4 (row, column) elements received."""
+    addr = [lane_address(slot_fn, l, kk, j, m0) for l in range(64)]
+    out = []
+    for l in range(64):
+        g0, i = (l // 16) * 16, l % 16
+        elems = []
+        for q in range(4):
+            _, (r, m) = addr[g0 + i // 4 + 4 * q]
+            elems.append((r, m + i % 4))          # element i mod 4 of that lane's 8-byte piece
+        out.append(elems)
+    return out
+
+
+def test_xor_patterns_are_bijections():
+    for r in range(64):
+        assert sorted(c ^ krow_xor(r) for c in range(32)) == list(range(32))
+    for c in range(32):
+        assert sorted(r ^ cm_xor(c) for r in range(64)) == list(range(64))
+
+
+def test_transposed_reads_deliver_mfma_fragments():
+    for slot_fn in (slot_krow, slot_cm):
+        for kk in range(4):
+            for m0 in range(0, 256, 32):
+                got = [transposed_read(slot_fn, kk, j, m0) for j in range(2)]
+                for l in range(64):
+                    frag = got[0][l] + got[1][l]
+                    want = [(16 * kk + 8 * (l >> 5) + t, m0 + (l & 31)) for t in range(8)]
+                    assert frag == want, (slot_fn.__name__, kk, m0, l)
+
+
+def test_transposed_reads_are_bank_conflict_free():
+    # 64 banks x 4 bytes; a request set is conflict-free when no two lanes
+    # touch different addresses in the same bank within one served group
+    for slot_fn in (slot_krow, slot_cm):
+        for kk in range(4):
+            for m0 in range(0, 256, 32):
+                for j in range(2):
+                    addrs = [lane_address(slot_fn, l, kk, j, m0)[0] for l in range(64)]
+                    for width, group in ((128, 16), (256, 32)):   # bytes per clock, lanes served together
+                        for g0 in range(0, 64, group):
+                            seen = {}
+                            for a in addrs[g0:g0 + group]:
+                                for b in range(a, a + 8, 4):
+                                    bank = (b % width) // 4
+                                    assert seen.setdefault(bank, b) == b, (slot_fn.__name__, width, kk, m0, j)
