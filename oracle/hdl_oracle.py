@@ -39,6 +39,20 @@ respect to the final hidden states and the lm-head weight follow from
 d log p_n(y) / d z_n[v] = 1[v == y] - p_n(v).  Masked rows contribute
 nothing and get a zero gradient; a token outside [0, V) has no indicator term.
 
+Entropy baseline (Sec. 4.1, "Rollout protocols"; Table 4): the next-token
+entropy -sum_v p(v) log p(v) of the same distributions under the original
+context, ranked per root like s (`select_by_value`).
+
+Group construction (Sec. 3 and 3.3, Sec. 4.1 "Training" and "Rollout
+protocols", Sec. 4.3-4.4): selection under an allowed index range and a
+minimum spacing (`select_constrained`), continuation slots per retained point
+(`allocate_continuations`), mean-centred group advantages
+(`group_advantages`), and the per-token derivative of the asymmetrically
+clipped surrogate with suffix-only training of continuations
+(`policy_loss_grad`).  Where the paper leaves values open (the constraint
+values, which point gets more continuations, a root with no valid point)
+they are parameters; the readings are listed in the design notes.
+
 Pins: every function here is checked by tests that do not re-type its formula
 (brute-force softmax with exact summation, closed forms, invariants, hand-worked
 fixtures, brute-force sorting).  See tests/test_oracle_pins.py.
