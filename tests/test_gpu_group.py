@@ -129,3 +129,55 @@ def test_policy_loss_grad(hdl):
     assert np.allclose(g[ok], og[ok], rtol=1e-5, atol=1e-12)
     assert np.allclose(l[ok], ol[ok], rtol=1e-5, atol=1e-12)
     assert np.all(g[(mask == 0) | (traj >= n_traj)] == 0.0)
+
+
+def test_group_construction_full_size(hdl):
+    # the benchmark's configuration (one training step at the paper's batch:
+    # 128 groups of 2 roots + 14 continuations, T = 4096, spacing 64, range
+    # excluding the first and last 32 positions): selection and allocation
+    # bit-exact, advantages within 1e-6, and the per-token factors of a seeded
+    # sample of the 8.4 million tokens against the oracle
+    n_groups, rpg, alloc, T = 128, 2, (3, 4), 4096
+    R = n_groups * rpg
+    lo_, hi_, mask = workloads.make_logp_pair(R, T, seed=1002 + 11)
+    L = np.full(R, 32, np.int32)
+    H = np.full(R, T - 33, np.int32)
+    idx, score, count = hdl.select_constrained(_t(lo_), _t(hi_), _t(mask), len(alloc), lo=_t(L), hi=_t(H),
+                                               min_gap=64)
+    bpos, brank = hdl.allocate_continuations(idx, count, alloc)
+    torch.cuda.synchronize()
+    oi, osc, oc = O.select_constrained(lo_, hi_, mask, len(alloc), lo=L, hi=H, min_gap=64, precision="f32")
+    assert np.array_equal(count.cpu().numpy(), oc) and np.array_equal(idx.cpu().numpy(), oi)
+    opos, orank = O.allocate_continuations(oi, oc, alloc)
+    assert np.array_equal(bpos.cpu().numpy(), opos) and np.array_equal(brank.cpu().numpy(), orank)
+
+    G = rpg * (1 + sum(alloc))
+    n_traj = n_groups * G
+    rng = np.random.default_rng(1002 + 12)
+    rewards = (rng.random((n_groups, G)) < 0.5).astype(np.float32)
+    adv = hdl.group_advantages(_t(rewards)).view(-1)
+    oadv = O.group_advantages(rewards).reshape(-1)
+    assert np.abs(adv.cpu().double().numpy() - oadv).max() <= 1e-6
+    n_tok = n_traj * T
+    traj = np.repeat(np.arange(n_traj, dtype=np.int32), T)
+    pos = np.tile(np.arange(T, dtype=np.int32), n_traj)
+    lo_old = (-rng.exponential(2.0, n_tok)).astype(np.float32)
+    lo_new = (lo_old + rng.normal(size=n_tok).astype(np.float32) * 0.2).astype(np.float32)
+    tmask = (rng.random(n_tok) < 0.9).astype(np.uint8)
+    start = np.zeros((n_groups, G), np.int32)
+    start[:, rpg:] = opos.reshape(n_groups, -1)
+    start = start.reshape(-1)
+    g, l = hdl.policy_loss_grad(adv, _t(traj), _t(lo_new), _t(lo_old), loss_mask=_t(tmask), pos=_t(pos),
+                                start=_t(start), scale=1.0 / n_tok)
+    torch.cuda.synchronize()
+    s = np.sort(rng.choice(n_tok, 200000, replace=False))
+    og, ol = O.policy_loss_grad(oadv, traj[s], lo_new[s], lo_old[s], tmask[s], pos[s], start,
+                                0.2, 0.28, 1.0 / n_tok)
+    gs, ls = g.cpu().double().numpy()[s], l.cpu().double().numpy()[s]
+    r = np.exp(lo_new[s].astype(np.float64) - lo_old[s].astype(np.float64))
+    ok = ~((np.abs(r - 0.8) < 1e-5) | (np.abs(r - 1.28) < 1e-5))
+    assert np.allclose(gs[ok], og[ok], rtol=1e-5, atol=1e-15)
+    assert np.allclose(ls[ok], ol[ok], rtol=1e-5, atol=1e-15)
+    # a continuation's reused prefix trains nothing
+    pre = pos[s] < start[traj[s]]
+    assert pre.any() and np.all(gs[pre] == 0.0)
