@@ -12,8 +12,15 @@ first 32 positions of each root excluded, k=8.
 Prints one JSON line:  value = scored tokens/s (both contexts), plus the
 fused kernel's roofline (achieved TFLOP/s of algorithmic 2*d*V flops per
 scored token over its HIP-event-timed duration, against the 2.5 PFLOP/s
-dense bf16 MFMA peak) and the float64 oracle timed on a bounded sample on
-the host cores.
+dense bf16 MFMA peak; HBM traffic from the committed rocprofv3 counters;
+for reference, this GPU's measured MFMA ceilings and the vendor GEMM on the
+same contraction) and the float64 oracle timed on a bounded sample on the
+host cores.
+
+Other passes: --selector entropy (the Entropy baseline's pass over the
+original context), --backward (gradients of a token-level loss through the
+lm-head), --group (group construction at the paper's batch).  --gpus N with
+N > 1 is refused: the path runs on one GPU.
 """
 from __future__ import annotations
 
