@@ -54,6 +54,20 @@ def build_ceiling_tool(verbose: bool = False) -> str:
     return CEILING_PATH
 
 
+ABI_CHECK_PATH = os.path.join(PKG_DIR, "abi_check")
+
+
+def build_abi_check(verbose: bool = False) -> str:
+    """A native C++ consumer of the C ABI (no Python): links libhdl.so,
+    which must be built first; finds it next to itself at run time."""
+    tmp = ABI_CHECK_PATH + ".tmp"
+    _hipcc(["-O2", "-std=c++17", "-Wall", "-I", os.path.join(ROOT, "include"),
+            os.path.join(PKG_DIR, "csrc", "tools", "abi_check.cpp"),
+            "-L", PKG_DIR, "-lhdl", "-Wl,-rpath,$ORIGIN", "-o", tmp], verbose)
+    os.replace(tmp, ABI_CHECK_PATH)
+    return ABI_CHECK_PATH
+
+
 def build_library(verbose: bool = False) -> str:
     tmp = LIB_PATH + ".tmp"
     _hipcc([*HIP_FLAGS, "-I", os.path.join(ROOT, "include"), *sources(), "-o", tmp], verbose)
@@ -64,3 +78,4 @@ def build_library(verbose: bool = False) -> str:
 if __name__ == "__main__":
     print(build_library(verbose=True))
     print(build_ceiling_tool(verbose=True))
+    print(build_abi_check(verbose=True))
