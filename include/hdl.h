@@ -15,6 +15,8 @@
  *  - Work is enqueued asynchronously on `stream` (a hipStream_t; NULL means
  *    the default stream).  Outputs are valid once the caller synchronises the
  *    stream.  The library never synchronises.
+ *  - Kernels launch on the calling thread's current HIP device; `stream` and
+ *    every pointer must belong to that device.
  *  - Argument errors are reported synchronously by a negative return value,
  *    before anything is enqueued.  A failed kernel launch returns
  *    HDL_ERR_HIP.  hdl_last_error() describes the most recent failure of the
