@@ -66,35 +66,69 @@ __global__ __launch_bounds__(256) void advantages_kernel(const float* __restrict
   for (int j = threadIdx.x; j < group_size; j += 256) adv[g * group_size + j] = R[j] - mean;
 }
 
-__global__ __launch_bounds__(256) void policy_grad_kernel(const float* __restrict__ adv,
-                                                          const int32_t* __restrict__ traj,
-                                                          const int32_t* __restrict__ pos,
-                                                          const int32_t* __restrict__ start,
-                                                          const float* __restrict__ logp_new,
-                                                          const float* __restrict__ logp_old,
-                                                          const uint8_t* __restrict__ loss_mask,
-                                                          int64_t n_tokens, int64_t n_traj, float eps_low,
-                                                          float eps_high,
-                                                          float scale, float* __restrict__ grad,
-                                                          float* __restrict__ loss) {
-  const int64_t n = static_cast<int64_t>(blockIdx.x) * blockDim.x + threadIdx.x;
-  if (n >= n_tokens) return;
-  const int32_t j = traj[n];
-  bool on = (loss_mask == nullptr || loss_mask[n] != 0) && j >= 0 && j < n_traj;
-  if (pos && start) on = on && pos[n] >= start[j];
-  float gv = 0.f, lv = 0.f;
+struct PolicyGradArgs {
+  const float* adv;
+  const int32_t* traj;
+  const int32_t* pos;
+  const int32_t* start;
+  const float* logp_new;
+  const float* logp_old;
+  const uint8_t* loss_mask;
+  int64_t n_tokens, n_traj;
+  float eps_low, eps_high, scale;
+  float* grad;
+  float* loss;
+};
+
+// One token's factor; m is the token's loss-mask byte (1 when there is no mask).
+__device__ __forceinline__ void token_factor(const PolicyGradArgs& p, int32_t j, int32_t pos, uint8_t m,
+                                             float ln, float lo, float& gv, float& lv) {
+  bool on = m != 0 && j >= 0 && j < p.n_traj;
+  if (p.pos && p.start) on = on && pos >= p.start[j];
+  gv = 0.f;
+  lv = 0.f;
   if (on) {
-    const float a = adv[j];
-    const float r = expf(logp_new[n] - logp_old[n]);
-    const float rc = fminf(fmaxf(r, 1.f - eps_low), 1.f + eps_high);
+    const float a = p.adv[j];
+    const float r = expf(ln - lo);
+    const float rc = fminf(fmaxf(r, 1.f - p.eps_low), 1.f + p.eps_high);
     const float unclipped = r * a, clipped = rc * a;
     // d/dlog pi of min(r A, clip(r) A): r A where the unclipped term is the
     // minimum (ties included), 0 where the clipped constant is
-    gv = unclipped <= clipped ? -a * r * scale : 0.f;
-    lv = -fminf(unclipped, clipped) * scale;
+    gv = unclipped <= clipped ? -a * r * p.scale : 0.f;
+    lv = -fminf(unclipped, clipped) * p.scale;
   }
-  grad[n] = gv;
-  if (loss) loss[n] = lv;
+}
+
+// VEC = 4: four consecutive tokens per thread through 16-byte loads and
+// stores (every per-token array 16-byte aligned, the mask 4-byte aligned);
+// VEC = 1: one token per thread, any alignment.
+template <int VEC>
+__global__ __launch_bounds__(256) void policy_grad_kernel(PolicyGradArgs p) {
+  const int64_t n0 = (static_cast<int64_t>(blockIdx.x) * blockDim.x + threadIdx.x) * VEC;
+  if (n0 >= p.n_tokens) return;
+  if (VEC == 4 && n0 + 4 <= p.n_tokens) {
+    const int4 j = *reinterpret_cast<const int4*>(p.traj + n0);
+    const int4 ps = p.pos ? *reinterpret_cast<const int4*>(p.pos + n0) : make_int4(0, 0, 0, 0);
+    const float4 ln = *reinterpret_cast<const float4*>(p.logp_new + n0);
+    const float4 lo = *reinterpret_cast<const float4*>(p.logp_old + n0);
+    const uchar4 m = p.loss_mask ? *reinterpret_cast<const uchar4*>(p.loss_mask + n0) : make_uchar4(1, 1, 1, 1);
+    float4 g, l;
+    token_factor(p, j.x, ps.x, m.x, ln.x, lo.x, g.x, l.x);
+    token_factor(p, j.y, ps.y, m.y, ln.y, lo.y, g.y, l.y);
+    token_factor(p, j.z, ps.z, m.z, ln.z, lo.z, g.z, l.z);
+    token_factor(p, j.w, ps.w, m.w, ln.w, lo.w, g.w, l.w);
+    *reinterpret_cast<float4*>(p.grad + n0) = g;
+    if (p.loss) *reinterpret_cast<float4*>(p.loss + n0) = l;
+    return;
+  }
+  const int64_t n1 = n0 + VEC < p.n_tokens ? n0 + VEC : p.n_tokens;
+  for (int64_t n = n0; n < n1; ++n) {
+    float gv, lv;
+    token_factor(p, p.traj[n], p.pos ? p.pos[n] : 0, p.loss_mask ? p.loss_mask[n] : 1, p.logp_new[n],
+                 p.logp_old[n], gv, lv);
+    p.grad[n] = gv;
+    if (p.loss) p.loss[n] = lv;
+  }
 }
 
 }  // namespace
@@ -121,10 +155,18 @@ hipError_t launch_policy_grad(const float* adv, const int32_t* traj, const int32
                               const float* logp_new, const float* logp_old, const uint8_t* loss_mask,
                               int64_t n_tokens, int64_t n_traj, float eps_low, float eps_high, float scale,
                               float* grad, float* loss, hipStream_t stream) {
-  const int64_t blocks = (n_tokens + 255) / 256;
-  hipLaunchKernelGGL(policy_grad_kernel, dim3(static_cast<unsigned>(blocks)), dim3(256), 0, stream, adv, traj,
-                     pos, start, logp_new, logp_old, loss_mask, n_tokens, n_traj, eps_low, eps_high, scale, grad,
-                     loss);
+  const PolicyGradArgs a{adv, traj, pos, start, logp_new, logp_old, loss_mask, n_tokens, n_traj,
+                         eps_low, eps_high, scale, grad, loss};
+  auto al = [](const void* q, uintptr_t b) { return q == nullptr || reinterpret_cast<uintptr_t>(q) % b == 0; };
+  const bool vec = al(traj, 16) && al(pos, 16) && al(logp_new, 16) && al(logp_old, 16) && al(grad, 16) &&
+                   al(loss, 16) && al(loss_mask, 4);
+  if (vec) {
+    const int64_t blocks = (n_tokens + 1023) / 1024;
+    hipLaunchKernelGGL(policy_grad_kernel<4>, dim3(static_cast<unsigned>(blocks)), dim3(256), 0, stream, a);
+  } else {
+    const int64_t blocks = (n_tokens + 255) / 256;
+    hipLaunchKernelGGL(policy_grad_kernel<1>, dim3(static_cast<unsigned>(blocks)), dim3(256), 0, stream, a);
+  }
   return hipGetLastError();
 }
 

@@ -181,3 +181,30 @@ def test_group_construction_full_size(hdl):
     # a continuation's reused prefix trains nothing
     pre = pos[s] < start[traj[s]]
     assert pre.any() and np.all(gs[pre] == 0.0)
+
+
+def test_policy_loss_grad_tail_and_unaligned(hdl):
+    # 1001 tokens: the four-per-thread path with a ragged tail; the same data
+    # as views one element into their buffers (not 16-byte aligned): the
+    # one-per-thread path.  Both against the oracle.
+    rng = np.random.default_rng(21)
+    n_traj, n = 7, 1001
+    adv = rng.normal(size=n_traj).astype(np.float32)
+    traj = rng.integers(0, n_traj, n + 1).astype(np.int32)
+    lo_ = (rng.normal(size=n + 1) * 0.5 - 2).astype(np.float32)
+    ln = (lo_ + rng.normal(size=n + 1) * 0.3).astype(np.float32)
+    mask = (rng.random(n + 1) < 0.8).astype(np.uint8)
+    pos = (np.arange(n + 1) % 300).astype(np.int32)
+    start = rng.integers(0, 150, n_traj).astype(np.int32)
+    for off in (0, 1):
+        sl = slice(off, off + n)
+        args = [_t(traj)[sl], _t(ln)[sl], _t(lo_)[sl]]
+        g, l = hdl.policy_loss_grad(_t(adv), *args, loss_mask=_t(mask)[sl], pos=_t(pos)[sl], start=_t(start),
+                                    scale=0.01)
+        torch.cuda.synchronize()
+        og, ol = O.policy_loss_grad(adv, traj[sl], ln[sl], lo_[sl], mask[sl], pos[sl], start, 0.2, 0.28, 0.01)
+        r = np.exp(ln[sl].astype(np.float64) - lo_[sl].astype(np.float64))
+        ok = ~((np.abs(r - 0.8) < 1e-5) | (np.abs(r - 1.28) < 1e-5))
+        gg, ll = g.cpu().double().numpy(), l.cpu().double().numpy()
+        assert np.allclose(gg[ok], og[ok], rtol=1e-5, atol=1e-12), f"offset {off}"
+        assert np.allclose(ll[ok], ol[ok], rtol=1e-5, atol=1e-12), f"offset {off}"
