@@ -184,9 +184,9 @@ size_t hdl_token_logprobs_backward_workspace_size(int64_t n_rows, int64_t d, int
  * contractions run on bf16 MFMA tiles with fp32 accumulation.
  *
  *  hidden, w_vocab, tokens, mask, n_rows, d, vocab: as for hdl_token_logprobs;
- *               dtype must be HDL_BF16.  Hidden states must not exceed 4 GiB,
- *               vocab must not exceed 2^30 and d 2^23
- *               (HDL_ERR_UNSUPPORTED otherwise).
+ *               dtype must be HDL_BF16; vocab must not exceed 2^30 and d
+ *               2^23 (HDL_ERR_UNSUPPORTED otherwise).  Hidden states over
+ *               4 GiB are processed in blocks of rows internally.
  *  lse          [n_rows] fp32: the log-sum-exp hdl_token_logprobs returned
  *               for the same inputs (read for scored rows only).
  *  grad_logp    [n_rows] fp32: g_n (read for scored rows only).

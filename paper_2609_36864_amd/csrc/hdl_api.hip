@@ -414,8 +414,9 @@ size_t hdl_token_logprobs_backward_workspace_size(int64_t n_rows, int64_t d, int
   if (n_rows <= 0 || d <= 0 || vocab <= 0 || n_rows > INT32_MAX || vocab > INT32_MAX) return 0;
   if (dtype != HDL_BF16 || d % 8 != 0) return 0;
   if (vocab > kBwdMaxVocab || d > kBwdMaxD) return 0;
-  if (hdl::rows_per_launch(d, 2) < n_rows) return 0;
-  return make_bwd_plan(n_rows, vocab, d).bytes;
+  const int64_t rpl = hdl::rows_per_launch(d, 2);
+  if (rpl < hdl::kTileN) return 0;
+  return make_bwd_plan(n_rows < rpl ? n_rows : rpl, vocab, d).bytes;
 }
 
 int hdl_token_logprobs_backward(const void* hidden, const void* w_vocab, const int32_t* tokens,
@@ -438,11 +439,14 @@ int hdl_token_logprobs_backward(const void* hidden, const void* w_vocab, const i
   if (vocab > kBwdMaxVocab || d > kBwdMaxD)
     return fail(HDL_ERR_UNSUPPORTED, "%s: vocab must not exceed %lld and d %lld", fn,
                 static_cast<long long>(kBwdMaxVocab), static_cast<long long>(kBwdMaxD));
-  if (hdl::rows_per_launch(d, 2) < n_rows)
-    return fail(HDL_ERR_UNSUPPORTED, "%s: hidden states larger than 4 GiB", fn);
+  // Rows are taken in blocks whose hidden states span at most 4 GiB (the
+  // kernels address a block's rows with 32-bit byte offsets).
+  const int64_t rpl = hdl::rows_per_launch(d, 2);
+  if (rpl < hdl::kTileN) return fail(HDL_ERR_UNSUPPORTED, "%s: d=%lld too large", fn, static_cast<long long>(d));
   if (!aligned(hidden, 16) || !aligned(w_vocab, 16) || !aligned(grad_hidden, 16) || !aligned(grad_w, 16))
     return fail(HDL_ERR_INVALID_ARG, "%s: hidden, w_vocab, grad_hidden and grad_w must be 16-byte aligned", fn);
-  const BwdPlan plan = make_bwd_plan(n_rows, vocab, d);
+  const int64_t block_rows = n_rows < rpl ? n_rows : rpl;
+  const BwdPlan plan = make_bwd_plan(block_rows, vocab, d);
   if (!workspace || workspace_bytes < plan.bytes)
     return fail(HDL_ERR_WORKSPACE, "%s: workspace of %zu bytes needed, %zu given", fn, plan.bytes,
                 workspace ? workspace_bytes : static_cast<size_t>(0));
@@ -457,68 +461,82 @@ int hdl_token_logprobs_backward(const void* hidden, const void* w_vocab, const i
   uint16_t* hc = reinterpret_cast<uint16_t*>(ws + plan.off_hc);
   float* hpart = reinterpret_cast<float*>(ws + plan.off_hpart);
 
-  hipError_t e = hdl::launch_compact(mask, n_rows, rows, n_scored, nullptr, nullptr, nullptr, s);
-  if (e != hipSuccess) return hip_fail(e, "compaction launch");
-  if ((e = hdl::launch_zero_masked_rows(mask, n_rows, d, grad_hidden, s)) != hipSuccess)
-    return hip_fail(e, "row clearing launch");
-  for (int64_t c = 0; c < plan.n_chunks; ++c) {
-    const int64_t base = c * plan.nc;
-    // 1. G for this chunk's scored rows (logits recomputed tile by tile)
-    hdl::LmheadArgs a{};
-    a.hidden = hidden;
-    a.w = w_vocab;
-    a.tokens = tokens;
-    a.rows = rows + base;
-    a.n_scored = n_scored;
-    a.d = d;
-    a.vocab = vocab;
-    a.n_vt = plan.fwd.n_vt;
-    a.tpc = plan.fwd.tpc;
-    a.n_ch = plan.fwd.n_ch;
-    a.n_grt = plan.fwd.n_grt;
-    a.row_base = base;
-    a.row_cap = plan.nc;
-    a.lse_in = lse;
-    a.grad_in = grad_logp;
-    a.g_out = g;
-    a.g_ld = plan.nc;   // chunk-major: nc rows per 8-column plane
-    a.g_cols = plan.v_pad;
-    TimedLaunch tg_;
-    if ((e = tg_.start(s)) != hipSuccess) return hip_fail(e, "timing event");
-    if ((e = hdl::launch_lmhead_grad(a, plan.fwd.grid, s)) != hipSuccess) return hip_fail(e, "gradient kernel launch");
-    if ((e = tg_.stop(HDL_PROFILE_GRAD, s)) != hipSuccess) return hip_fail(e, "timing event");
-    // 2. the chunk's scored hidden rows, gathered (zeros up to the next 64 rows)
-    if ((e = hdl::launch_gather_rows(static_cast<const uint16_t*>(hidden), d, rows + base, n_scored, base, plan.nc,
-                                     d, hc, s)) != hipSuccess)
-      return hip_fail(e, "row gather launch");
-    // 3. dH rows of the chunk: G W (W read as stored, K = vocabulary rows past
-    // V clamped: G is zero there), split along the vocabulary, partials summed in order
-    hdl::GemmArgs gh = gemm_args(g, plan.nc, hdl::kLayoutCmRow, 0, 0, w_vocab, d, d, vocab, plan.nc, d, plan.v_pad,
-                                 hpart, d);
-    gh.dyn = n_scored;
-    gh.dyn_base = base;
-    gh.dyn_dim = 1;
-    gh.k_split = plan.k_split;
-    gh.splits = plan.splits;
-    gh.c_split_stride = plan.nc * d;
-    TimedLaunch th_;
-    if ((e = th_.start(s)) != hipSuccess) return hip_fail(e, "timing event");
-    if ((e = hdl::launch_gemm(gh, s)) != hipSuccess) return hip_fail(e, "GEMM launch");
-    if ((e = th_.stop(HDL_PROFILE_GEMM, s)) != hipSuccess) return hip_fail(e, "timing event");
-    if ((e = hdl::launch_splitk_scatter(hpart, plan.splits, plan.nc * d, d, rows + base, n_scored, base, plan.nc,
-                                        grad_hidden, s)) != hipSuccess)
-      return hip_fail(e, "split-K sum launch");
-    // 4. dW (+)= G^T H over the chunk's rows (both read with the row index as K)
-    hdl::GemmArgs gw = gemm_args(g, plan.nc, hdl::kLayoutCmKRow, plan.v_pad, plan.nc, hc, d, d, plan.nc, vocab, d,
-                                 plan.nc, grad_w, d);
-    gw.dyn = n_scored;
-    gw.dyn_base = base;
-    gw.dyn_dim = 2;
-    gw.beta = (c > 0 || accumulate_w) ? 1 : 0;
-    TimedLaunch tw_;
-    if ((e = tw_.start(s)) != hipSuccess) return hip_fail(e, "timing event");
-    if ((e = hdl::launch_gemm(gw, s)) != hipSuccess) return hip_fail(e, "GEMM launch");
-    if ((e = tw_.stop(HDL_PROFILE_GEMM, s)) != hipSuccess) return hip_fail(e, "timing event");
+  hipError_t e = hipSuccess;
+  for (int64_t b0 = 0; b0 < n_rows; b0 += block_rows) {
+    // one block of rows: every pointer below is offset to the block
+    const int64_t nb = n_rows - b0 < block_rows ? n_rows - b0 : block_rows;
+    const uint8_t* mask_b = mask ? mask + b0 : nullptr;
+    const void* hidden_b = static_cast<const char*>(hidden) + b0 * d * 2;
+    const int32_t* tokens_b = tokens + b0;
+    const float* lse_b = lse + b0;
+    const float* grad_b = grad_logp + b0;
+    float* dh_b = grad_hidden + b0 * d;
+    if ((e = hdl::launch_compact(mask_b, nb, rows, n_scored, nullptr, nullptr, nullptr, s)) != hipSuccess)
+      return hip_fail(e, "compaction launch");
+    if ((e = hdl::launch_zero_masked_rows(mask_b, nb, d, dh_b, s)) != hipSuccess)
+      return hip_fail(e, "row clearing launch");
+    const int64_t n_chunks = (nb + plan.nc - 1) / plan.nc;
+    for (int64_t c = 0; c < n_chunks; ++c) {
+      const int64_t base = c * plan.nc;
+      // 1. G for this chunk's scored rows (logits recomputed tile by tile)
+      hdl::LmheadArgs a{};
+      a.hidden = hidden_b;
+      a.w = w_vocab;
+      a.tokens = tokens_b;
+      a.rows = rows + base;
+      a.n_scored = n_scored;
+      a.d = d;
+      a.vocab = vocab;
+      a.n_vt = plan.fwd.n_vt;
+      a.tpc = plan.fwd.tpc;
+      a.n_ch = plan.fwd.n_ch;
+      a.n_grt = plan.fwd.n_grt;
+      a.row_base = base;
+      a.row_cap = plan.nc;
+      a.lse_in = lse_b;
+      a.grad_in = grad_b;
+      a.g_out = g;
+      a.g_ld = plan.nc;   // chunk-major: nc rows per 8-column plane
+      a.g_cols = plan.v_pad;
+      TimedLaunch tg_;
+      if ((e = tg_.start(s)) != hipSuccess) return hip_fail(e, "timing event");
+      if ((e = hdl::launch_lmhead_grad(a, plan.fwd.grid, s)) != hipSuccess)
+        return hip_fail(e, "gradient kernel launch");
+      if ((e = tg_.stop(HDL_PROFILE_GRAD, s)) != hipSuccess) return hip_fail(e, "timing event");
+      // 2. the chunk's scored hidden rows, gathered (zeros up to the next 64 rows)
+      if ((e = hdl::launch_gather_rows(static_cast<const uint16_t*>(hidden_b), d, rows + base, n_scored, base,
+                                       plan.nc, d, hc, s)) != hipSuccess)
+        return hip_fail(e, "row gather launch");
+      // 3. dH rows of the chunk: G W (W read as stored, K = vocabulary rows past
+      // V clamped: G is zero there), split along the vocabulary, partials summed in order
+      hdl::GemmArgs gh = gemm_args(g, plan.nc, hdl::kLayoutCmRow, 0, 0, w_vocab, d, d, vocab, plan.nc, d,
+                                   plan.v_pad, hpart, d);
+      gh.dyn = n_scored;
+      gh.dyn_base = base;
+      gh.dyn_dim = 1;
+      gh.k_split = plan.k_split;
+      gh.splits = plan.splits;
+      gh.c_split_stride = plan.nc * d;
+      TimedLaunch th_;
+      if ((e = th_.start(s)) != hipSuccess) return hip_fail(e, "timing event");
+      if ((e = hdl::launch_gemm(gh, s)) != hipSuccess) return hip_fail(e, "GEMM launch");
+      if ((e = th_.stop(HDL_PROFILE_GEMM, s)) != hipSuccess) return hip_fail(e, "timing event");
+      if ((e = hdl::launch_splitk_scatter(hpart, plan.splits, plan.nc * d, d, rows + base, n_scored, base,
+                                          plan.nc, dh_b, s)) != hipSuccess)
+        return hip_fail(e, "split-K sum launch");
+      // 4. dW (+)= G^T H over the chunk's rows (both read with the row index as
+      // K); the call's first chunk overwrites dW unless the caller accumulates
+      hdl::GemmArgs gw = gemm_args(g, plan.nc, hdl::kLayoutCmKRow, plan.v_pad, plan.nc, hc, d, d, plan.nc, vocab,
+                                   d, plan.nc, grad_w, d);
+      gw.dyn = n_scored;
+      gw.dyn_base = base;
+      gw.dyn_dim = 2;
+      gw.beta = (b0 > 0 || c > 0 || accumulate_w) ? 1 : 0;
+      TimedLaunch tw_;
+      if ((e = tw_.start(s)) != hipSuccess) return hip_fail(e, "timing event");
+      if ((e = hdl::launch_gemm(gw, s)) != hipSuccess) return hip_fail(e, "GEMM launch");
+      if ((e = tw_.stop(HDL_PROFILE_GEMM, s)) != hipSuccess) return hip_fail(e, "timing event");
+    }
   }
   return HDL_OK;
 }

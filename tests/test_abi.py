@@ -106,6 +106,9 @@ def test_backward_workspace_and_argument_errors(lib):
     assert ws(n, d, 1 << 23, 1) > 0 and ws(n, d, (1 << 30) + 1, 1) == 0   # vocabulary limit
     # G is held for one chunk of at most 32768 rows: more rows only lengthen the row list
     assert 0 < ws(100000, d, V, 1) - ws(32768, d, V, 1) < 4 * 100000
+    # rows are taken in blocks whose hidden states span at most 4 GiB, so the
+    # row list stops growing at 2^32 / (2 d) rows
+    assert ws(600000, 4096, V, 1) == ws(524288, 4096, V, 1) > ws(524287 - 32768, 4096, V, 1)
     assert ws(n, (1 << 23) + 8, V, 1) == 0
     assert ws(n, d, V, 0) == 0          # fp32 inputs are not supported
     assert ws(n, 12, V, 1) == 0         # d not a multiple of 8

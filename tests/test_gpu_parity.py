@@ -283,7 +283,8 @@ def test_boundary_errors(hdl):
 def test_hidden_states_over_4gib_split_into_launches(hdl):
     # 525,065 rows of d = 4096 bf16 (4.3 GB): the library cuts the call into
     # launches of 2^32 / 8192 = 524,288 rows (32-bit DMA offsets); rows on
-    # both sides of the cut must match the oracle and masked rows stay 0
+    # both sides of the cut must match the oracle and masked rows stay 0,
+    # in the forward and in the backward pass
     n, d, V = 524288 + 777, 4096, 1000
     gen = torch.Generator(device="cuda").manual_seed(77)
     H = torch.randn(n, d, device="cuda", generator=gen).to(torch.bfloat16)
@@ -300,12 +301,23 @@ def test_hidden_states_over_4gib_split_into_launches(hdl):
     on = mk != 0
     assert np.abs(got[on] - want[on]).max() <= TOL_BF16
     assert np.all(got[~on] == 0.0)
-    del H
-    torch.cuda.empty_cache()
-    # the backward pass keeps one launch and refuses this size
-    with pytest.raises(ValueError):
-        hdl.token_logprobs_backward(torch.zeros(n, d, dtype=torch.bfloat16, device="cuda"), W, y, m, lse,
-                                    torch.zeros(n, device="cuda"))
+    # the backward pass takes the same row blocks.  g is zero except on the
+    # sampled rows, so dW = sum over those rows of G_n^T h_n is the oracle's
+    # whole answer even though every row is processed; dH is zero elsewhere
+    gs = np.random.default_rng(5).normal(size=rows.size).astype(np.float32)
+    g = torch.zeros(n, device="cuda")
+    g[torch.as_tensor(rows, device="cuda")] = torch.from_numpy(gs).cuda()
+    prefill = torch.full((V, d), 1e3, device="cuda")       # overwritten: accumulate_w is off
+    dh, dw = hdl.token_logprobs_backward(H, W, y, m, lse, g, grad_w=prefill)
+    torch.cuda.synchronize()
+    nz = torch.nonzero((dh != 0).any(dim=1)).flatten().cpu().numpy()
+    assert set(nz.tolist()) <= set(rows[on].tolist())
+    want_dh, want_dw, mag_dh, mag_dw = O.token_logprobs_backward(
+        as_f64(Hs), as_f64(W.cpu()), y[torch.as_tensor(rows, device="cuda")].cpu().numpy(), gs, mk)
+    got_dh = dh[torch.as_tensor(rows, device="cuda")].cpu().double().numpy()
+    assert np.all(np.abs(got_dh - want_dh) <= 2.0 ** -8 * mag_dh + 1e-6 * mag_dh.max())
+    got_dw = dw.cpu().double().numpy()
+    assert np.all(np.abs(got_dw - want_dw) <= 2.0 ** -8 * mag_dw + 1e-6 * mag_dw.max())
 
 
 def test_weight_over_4gib(hdl):
