@@ -368,7 +368,7 @@ BwdPlan make_bwd_plan(int64_t n_rows, int64_t vocab, int64_t d) {
   off = round_up(off + sizeof(int32_t) * (64 + static_cast<size_t>((n_rows + 4095) / 4096)), 256);
   p.off_g = off;    // G chunk-major [v_pad / 8][nc][8] bf16
   off = round_up(off + 2 * static_cast<size_t>(p.nc) * static_cast<size_t>(p.v_pad), 256);
-  p.off_hc = off;   // the chunk's scored hidden rows, gathered [nc][d] bf16
+  p.off_hc = off;   // the chunk's scored hidden rows, gathered chunk-major [nc / 8][d][8] bf16
   off = round_up(off + 2 * static_cast<size_t>(p.nc) * static_cast<size_t>(d), 256);
   p.off_hpart = off;   // dH partial sums [splits][nc][d] fp32
   off = round_up(off + 4 * static_cast<size_t>(p.splits) * static_cast<size_t>(p.nc) * static_cast<size_t>(d), 256);
@@ -377,9 +377,10 @@ BwdPlan make_bwd_plan(int64_t n_rows, int64_t vocab, int64_t d) {
 }
 
 // Arguments of C = sum_k A(m, k) B(n, k): A is the chunk-major logit
-// gradient (layout a_layout), B is stored with K as its row.
+// gradient (layout a_layout), B is W stored with K as its row (kLayoutKRow)
+// or the gathered hidden rows, chunk-major along K (kLayoutCmRow).
 hdl::GemmArgs gemm_args(const void* a, int64_t lda, int a_layout, int64_t a_cols, int64_t a_krows, const void* b,
-                        int64_t ldb, int64_t b_cols, int64_t b_krows, int64_t m, int64_t n, int64_t k, float* c,
+                        int64_t ldb, int b_layout, int64_t b_cols, int64_t b_krows, int64_t m, int64_t n, int64_t k, float* c,
                         int64_t ldc) {
   hdl::GemmArgs g{};
   g.a = a;
@@ -389,7 +390,7 @@ hdl::GemmArgs gemm_args(const void* a, int64_t lda, int a_layout, int64_t a_cols
   g.a_krows = a_krows;
   g.b = b;
   g.ldb = ldb;
-  g.b_layout = hdl::kLayoutKRow;
+  g.b_layout = b_layout;
   g.b_cols = b_cols;
   g.b_krows = b_krows;
   g.m = m;
@@ -503,14 +504,15 @@ int hdl_token_logprobs_backward(const void* hidden, const void* w_vocab, const i
       if ((e = hdl::launch_lmhead_grad(a, plan.fwd.grid, s)) != hipSuccess)
         return hip_fail(e, "gradient kernel launch");
       if ((e = tg_.stop(HDL_PROFILE_GRAD, s)) != hipSuccess) return hip_fail(e, "timing event");
-      // 2. the chunk's scored hidden rows, gathered (zeros up to the next 64 rows)
-      if ((e = hdl::launch_gather_rows(static_cast<const uint16_t*>(hidden_b), d, rows + base, n_scored, base,
-                                       plan.nc, d, hc, s)) != hipSuccess)
+      // 2. the chunk's scored hidden rows, gathered chunk-major along the row
+      // index (zeros up to the next 64 rows)
+      if ((e = hdl::launch_gather_rows_cm(static_cast<const uint16_t*>(hidden_b), d, rows + base, n_scored, base,
+                                          plan.nc, d, hc, s)) != hipSuccess)
         return hip_fail(e, "row gather launch");
       // 3. dH rows of the chunk: G W (W read as stored, K = vocabulary rows past
       // V clamped: G is zero there), split along the vocabulary, partials summed in order
-      hdl::GemmArgs gh = gemm_args(g, plan.nc, hdl::kLayoutCmRow, 0, 0, w_vocab, d, d, vocab, plan.nc, d,
-                                   plan.v_pad, hpart, d);
+      hdl::GemmArgs gh = gemm_args(g, plan.nc, hdl::kLayoutCmRow, 0, 0, w_vocab, d, hdl::kLayoutKRow, d, vocab,
+                                   plan.nc, d, plan.v_pad, hpart, d);
       gh.dyn = n_scored;
       gh.dyn_base = base;
       gh.dyn_dim = 1;
@@ -526,8 +528,8 @@ int hdl_token_logprobs_backward(const void* hidden, const void* w_vocab, const i
         return hip_fail(e, "split-K sum launch");
       // 4. dW (+)= G^T H over the chunk's rows (both read with the row index as
       // K); the call's first chunk overwrites dW unless the caller accumulates
-      hdl::GemmArgs gw = gemm_args(g, plan.nc, hdl::kLayoutCmKRow, plan.v_pad, plan.nc, hc, d, d, plan.nc, vocab,
-                                   d, plan.nc, grad_w, d);
+      hdl::GemmArgs gw = gemm_args(g, plan.nc, hdl::kLayoutCmKRow, plan.v_pad, plan.nc, hc, d, hdl::kLayoutCmRow, 0,
+                                   0, vocab, d, plan.nc, grad_w, d);
       gw.dyn = n_scored;
       gw.dyn_base = base;
       gw.dyn_dim = 2;

@@ -106,12 +106,14 @@ hipError_t launch_compact(const uint8_t* mask, int64_t n_rows, int32_t* rows,
                           hipStream_t stream);
 hipError_t launch_lmhead(const LmheadArgs& a, int64_t grid, bool bf16, hipStream_t stream);
 hipError_t launch_lmhead_grad(const LmheadArgs& a, int64_t grid, hipStream_t stream);
-// Supported layouts (a, b): (kLayoutCmRow, kLayoutKRow), (kLayoutCmKRow, kLayoutKRow).
+// Supported layouts (a, b): (kLayoutCmRow, kLayoutKRow), (kLayoutCmKRow, kLayoutCmRow).
 hipError_t launch_gemm(const GemmArgs& a, hipStream_t stream);
-// out[e][:] = e < n ? in[map[e]][:] : 0 for e < min(round_up(n, 64), cap), where
-// n = clamp(*dyn - dyn_base, 0, cap); out is [cap][d] bf16, d % 8 == 0.
-hipError_t launch_gather_rows(const uint16_t* in, int64_t ld_in, const int32_t* map, const int32_t* dyn,
-                              int64_t dyn_base, int64_t cap, int64_t d, uint16_t* out, hipStream_t stream);
+// Row e < min(round_up(n, 64), cap) of X = (e < n ? in[map[e]][:] : 0), where
+// n = clamp(*dyn - dyn_base, 0, cap), stored chunk-major along e:
+// X[e][j] at ((e / 8) * d + j) * 8 + e % 8 (kLayoutCmRow with ld = d).
+// out holds cap * d bf16; d % 8 == 0, cap % 8 == 0.
+hipError_t launch_gather_rows_cm(const uint16_t* in, int64_t ld_in, const int32_t* map, const int32_t* dyn,
+                                 int64_t dyn_base, int64_t cap, int64_t d, uint16_t* out, hipStream_t stream);
 // dh[map[e]][j] = sum_s part[s][e][j] for e < clamp(*dyn - dyn_base, 0, cap)
 hipError_t launch_splitk_scatter(const float* part, int64_t splits, int64_t split_stride, int64_t d,
                                  const int32_t* map, const int32_t* dyn, int64_t dyn_base, int64_t cap,

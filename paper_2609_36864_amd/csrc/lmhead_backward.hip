@@ -13,10 +13,11 @@
 // (8 vocabulary entries of a row, then the same 8 of the next row).  The two
 // contractions are plain bf16 GEMMs on the same 256 x 256 MFMA tile as the
 // forward kernel (gemm_kernel below), each operand read as stored: G in
-// either role, W, and the chunk's hidden rows (gathered into a dense block by
-// gather_rows_kernel).  Operands whose stored rows run along the contracted
-// index are staged in LDS as stored and turned into MFMA fragments by
-// gfx950's transposing LDS reads, so nothing is transposed in memory.  dH is
+// either role, W, and the chunk's hidden rows (gathered into a dense block,
+// chunk-major along the row index, by gather_rows_cm_kernel).  Operands whose
+// stored rows run along the contracted index (W in dH, G in dW) are staged in
+// LDS as stored and turned into MFMA fragments by gfx950's transposing LDS
+// reads, so nothing large is transposed in memory.  dH is
 // split along the vocabulary when it has too few tiles for the chip, and its
 // partial sums are added in a fixed order (splitk_scatter_kernel): the whole
 // pass is deterministic.
@@ -322,23 +323,40 @@ __global__ __launch_bounds__(kThreads, 1) void gemm_kernel(GemmArgs p) {
   }
 }
 
-// out[e][:] = in[map[e]][:] for the e < n scored rows of the chunk, zeros for
-// n <= e < round_up(n, 64): the dense K-row operand of dW = G^T H.
-__global__ __launch_bounds__(256) void gather_rows_kernel(const uint16_t* __restrict__ in, int64_t ld_in,
-                                                          const int32_t* __restrict__ map,
-                                                          const int32_t* __restrict__ dyn, int64_t dyn_base,
-                                                          int64_t cap, int64_t d, uint16_t* __restrict__ out) {
+// The chunk's scored hidden rows, chunk-major along the row index (the dense
+// B operand of dW = G^T H with K = rows, read with plain 16-byte loads):
+// out[(e / 8) * d + j][e % 8] = in[map[e]][j] for the e < n scored rows,
+// zeros for n <= e < round_up(n, 64).  Each thread moves an 8 x 8 block
+// (8 rows x 8 columns): eight 16-byte row reads, eight 16-byte writes of one
+// column's 8 rows each.
+__global__ __launch_bounds__(256) void gather_rows_cm_kernel(const uint16_t* __restrict__ in, int64_t ld_in,
+                                                             const int32_t* __restrict__ map,
+                                                             const int32_t* __restrict__ dyn, int64_t dyn_base,
+                                                             int64_t cap, int64_t d, uint16_t* __restrict__ out) {
   int64_t n = *dyn - dyn_base;
   n = n < 0 ? 0 : (n > cap ? cap : n);
   int64_t n_pad = (n + 63) / 64 * 64;
   n_pad = n_pad < cap ? n_pad : cap;
-  const int64_t e = blockIdx.y;
-  if (e >= n_pad) return;
+  const int64_t e0 = static_cast<int64_t>(blockIdx.y) * 8;
+  if (e0 >= n_pad) return;
   const int64_t j = (static_cast<int64_t>(blockIdx.x) * 256 + threadIdx.x) * 8;
   if (j >= d) return;
-  uint4 v = make_uint4(0, 0, 0, 0);
-  if (e < n) v = *reinterpret_cast<const uint4*>(in + static_cast<int64_t>(map[e]) * ld_in + j);
-  *reinterpret_cast<uint4*>(out + e * d + j) = v;
+  uint4 rows[8];
+#pragma unroll
+  for (int r = 0; r < 8; ++r) {
+    rows[r] = make_uint4(0, 0, 0, 0);
+    if (e0 + r < n) rows[r] = *reinterpret_cast<const uint4*>(in + static_cast<int64_t>(map[e0 + r]) * ld_in + j);
+  }
+  const uint16_t* v = reinterpret_cast<const uint16_t*>(rows);   // v[r * 8 + c] = row r, column j + c
+  uint4* dst = reinterpret_cast<uint4*>(out + ((e0 / 8) * d + j) * 8);
+#pragma unroll
+  for (int c = 0; c < 8; ++c) {
+    uint32_t w[4];
+#pragma unroll
+    for (int q = 0; q < 4; ++q)
+      w[q] = static_cast<uint32_t>(v[(2 * q) * 8 + c]) | (static_cast<uint32_t>(v[(2 * q + 1) * 8 + c]) << 16);
+    dst[c] = make_uint4(w[0], w[1], w[2], w[3]);
+  }
 }
 
 // dh[map[e]][j] = sum over splits s (in order) of part[s][e][j].
@@ -380,18 +398,19 @@ hipError_t launch_gemm(const GemmArgs& a, hipStream_t stream) {
   const dim3 g(static_cast<unsigned>(grid)), blk(kThreads);
   if (a.a_layout == kLayoutCmRow && a.b_layout == kLayoutKRow)
     hipLaunchKernelGGL((gemm_kernel<kLayoutCmRow, kLayoutKRow>), g, blk, 0, stream, a);
-  else if (a.a_layout == kLayoutCmKRow && a.b_layout == kLayoutKRow)
-    hipLaunchKernelGGL((gemm_kernel<kLayoutCmKRow, kLayoutKRow>), g, blk, 0, stream, a);
+  else if (a.a_layout == kLayoutCmKRow && a.b_layout == kLayoutCmRow)
+    hipLaunchKernelGGL((gemm_kernel<kLayoutCmKRow, kLayoutCmRow>), g, blk, 0, stream, a);
   else
     return hipErrorInvalidValue;
   return hipGetLastError();
 }
 
-hipError_t launch_gather_rows(const uint16_t* in, int64_t ld_in, const int32_t* map, const int32_t* dyn,
-                              int64_t dyn_base, int64_t cap, int64_t d, uint16_t* out, hipStream_t stream) {
+hipError_t launch_gather_rows_cm(const uint16_t* in, int64_t ld_in, const int32_t* map, const int32_t* dyn,
+                                 int64_t dyn_base, int64_t cap, int64_t d, uint16_t* out, hipStream_t stream) {
   const int64_t gx = (d / 8 + 255) / 256;
-  if (gx <= 0 || cap <= 0) return hipSuccess;
-  hipLaunchKernelGGL(gather_rows_kernel, dim3(static_cast<unsigned>(gx), static_cast<unsigned>(cap)), dim3(256), 0,
+  const int64_t gy = (cap + 7) / 8;
+  if (gx <= 0 || gy <= 0) return hipSuccess;
+  hipLaunchKernelGGL(gather_rows_cm_kernel, dim3(static_cast<unsigned>(gx), static_cast<unsigned>(gy)), dim3(256), 0,
                      stream, in, ld_in, map, dyn, dyn_base, cap, d, out);
   return hipGetLastError();
 }
