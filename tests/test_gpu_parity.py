@@ -301,6 +301,15 @@ def test_hidden_states_over_4gib_split_into_launches(hdl):
     on = mk != 0
     assert np.abs(got[on] - want[on]).max() <= TOL_BF16
     assert np.all(got[~on] == 0.0)
+    # the entropy output goes through the same row blocks
+    lp2, _, ent = hdl.token_logprobs(H, W, y, m, want_entropy=True)
+    torch.cuda.synchronize()
+    assert torch.equal(lp2.view(torch.int32), lp.view(torch.int32))
+    got_ent = ent[torch.as_tensor(rows, device="cuda")].cpu().numpy()
+    want_ent = O.token_entropy(as_f64(Hs), as_f64(W.cpu()))
+    assert np.abs(got_ent[on] - want_ent[on]).max() <= TOL_BF16
+    assert np.all(got_ent[~on] == 0.0)
+    del lp2, ent
     # the backward pass takes the same row blocks.  g is zero except on the
     # sampled rows, so dW = sum over those rows of G_n^T h_n is the oracle's
     # whole answer even though every row is processed; dH is zero elsewhere
