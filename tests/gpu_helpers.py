@@ -14,7 +14,7 @@ def require_gpu():
     if not torch.cuda.is_available():
         pytest.skip("no GPU")
     import paper_2609_36864_amd as hdl
-    hdl.load_library()   # raises (test fails) if the library is missing on a GPU machine
+    hdl.load_library()   # raises (test fails) if the library is missing on a machine with a GPU
     return hdl
 
 
