@@ -309,6 +309,8 @@ def allocate_continuations(idx: np.ndarray, count: np.ndarray, alloc, fallback: 
     branches at `fallback`."""
     idx = np.asarray(idx)
     R, k = idx.shape
+    if len(alloc) != k:
+        raise ValueError("alloc needs one slot count per selected rank")
     total = int(sum(alloc))
     pos = np.zeros((R, total), dtype=np.int32)
     rank = np.zeros((R, total), dtype=np.int32)

@@ -570,6 +570,8 @@ def test_allocation_fixtures():
     # 2 x 1 configuration (Table 5): all seven at the single point
     pos, _ = O.allocate_continuations(np.array([[9]], np.int32), np.array([1]), (7,))
     assert pos[0].tolist() == [9] * 7
+    with pytest.raises(ValueError):   # one slot count per rank, as the C ABI requires
+        O.allocate_continuations(np.array([[9]], np.int32), np.array([1]), (3, 4))
 
 
 def test_group_advantages_closed_forms():
