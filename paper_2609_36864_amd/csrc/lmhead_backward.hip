@@ -347,16 +347,16 @@ __global__ __launch_bounds__(256) void gather_rows_cm_kernel(const uint16_t* __r
     rows[r] = make_uint4(0, 0, 0, 0);
     if (e0 + r < n) rows[r] = *reinterpret_cast<const uint4*>(in + static_cast<int64_t>(map[e0 + r]) * ld_in + j);
   }
-  const uint16_t* v = reinterpret_cast<const uint16_t*>(rows);   // v[r * 8 + c] = row r, column j + c
+  // element (r, c): 16-bit half c % 2 (low half first) of 32-bit word c / 2 of row r
+  auto elem = [&](int r, int c) -> uint32_t {
+    const uint32_t w = (c >> 1) == 0 ? rows[r].x : (c >> 1) == 1 ? rows[r].y : (c >> 1) == 2 ? rows[r].z : rows[r].w;
+    return (c & 1) ? (w >> 16) : (w & 0xffffu);
+  };
   uint4* dst = reinterpret_cast<uint4*>(out + ((e0 / 8) * d + j) * 8);
 #pragma unroll
-  for (int c = 0; c < 8; ++c) {
-    uint32_t w[4];
-#pragma unroll
-    for (int q = 0; q < 4; ++q)
-      w[q] = static_cast<uint32_t>(v[(2 * q) * 8 + c]) | (static_cast<uint32_t>(v[(2 * q + 1) * 8 + c]) << 16);
-    dst[c] = make_uint4(w[0], w[1], w[2], w[3]);
-  }
+  for (int c = 0; c < 8; ++c)
+    dst[c] = make_uint4(elem(0, c) | (elem(1, c) << 16), elem(2, c) | (elem(3, c) << 16),
+                        elem(4, c) | (elem(5, c) << 16), elem(6, c) | (elem(7, c) << 16));
 }
 
 // dh[map[e]][j] = sum over splits s (in order) of part[s][e][j].
