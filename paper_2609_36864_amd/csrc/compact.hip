@@ -17,6 +17,7 @@ namespace {
 constexpr int kThreads = 256;
 constexpr int kPerThread = 16;
 constexpr int kPerBlock = kThreads * kPerThread;   // 4096 rows per block
+static_assert(kPerBlock == kCountBlockRows, "the workspace holds one count per block");
 
 __device__ __forceinline__ int wave_incl_scan(int v) {
   const int lane = threadIdx.x & 63;
@@ -107,7 +108,7 @@ __global__ __launch_bounds__(kThreads) void scatter_kernel(const uint8_t* __rest
 }  // namespace
 
 // Scratch for the per-block counts lives right after n_scored in the
-// workspace (see make_plan in hdl_api.hip).
+// workspace (see layout_workspace in plan.h).
 hipError_t launch_compact(const uint8_t* mask, int64_t n_rows, int32_t* rows, int32_t* n_scored,
                           float* logp, float* lse, float* entropy, hipStream_t stream) {
   const int64_t blocks = (n_rows + kPerBlock - 1) / kPerBlock;

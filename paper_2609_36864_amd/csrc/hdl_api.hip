@@ -79,48 +79,6 @@ struct TimedLaunch {
 
 }  // namespace
 
-namespace hdl {
-
-int64_t rows_per_launch(int64_t d, int esz) {
-  const int64_t row_bytes = d * esz;
-  return ((int64_t{1} << 32) / row_bytes) / kTileN * kTileN;
-}
-
-LmheadPlan make_plan(int64_t n_rows_total, int64_t vocab, int64_t d, int esz) {
-  LmheadPlan p{};
-  p.rows_per_launch = rows_per_launch(d, esz);
-  const int64_t n_rows = n_rows_total < p.rows_per_launch ? n_rows_total : p.rows_per_launch;
-  p.n_rows = n_rows;
-  p.n_vt = (vocab + kTileV - 1) / kTileV;
-  p.n_rt_max = (n_rows + kTileN - 1) / kTileN;
-  // Vocabulary tiles per work item: long items amortise the per-item
-  // pipeline fill and partial write; short ones balance the tail across 256
-  // CUs.  Aim for about 32 items per CU (measured: at 16,384 rows this runs
-  // 6 % faster than 8 items per CU; at 65,536 rows both give 16 tiles).
-  int64_t tpc = (p.n_rt_max * p.n_vt) / 8192;
-  if (tpc < 1) tpc = 1;
-  if (tpc > 16) tpc = 16;
-  p.tpc = tpc;
-  p.n_ch = (p.n_vt + tpc - 1) / tpc;
-  p.n_grt = (p.n_rt_max + kGroupRT - 1) / kGroupRT;
-  p.n_gch = (p.n_ch + kGroupCH - 1) / kGroupCH;
-  const int64_t groups = p.n_grt * p.n_gch;
-  p.grid = (groups + kNumXcd - 1) / kNumXcd * kNumXcd * (kGroupRT * kGroupCH);
-  // workspace: rows [n_rows] | n_scored + block counts | partials [4][n_ch][n_rows]
-  // (max, sum of exp, sampled-token logit, and the entropy accumulator)
-  size_t off = 0;
-  p.off_rows = off;
-  off = round_up(off + sizeof(int32_t) * static_cast<size_t>(n_rows), 256);
-  p.off_count = off;
-  const size_t n_blocks = static_cast<size_t>((n_rows + 4095) / 4096);
-  off = round_up(off + sizeof(int32_t) * (64 + n_blocks), 256);
-  p.off_part = off;
-  off = round_up(off + 4 * sizeof(float) * static_cast<size_t>(p.n_ch) * static_cast<size_t>(n_rows), 256);
-  p.bytes = off;
-  return p;
-}
-
-}  // namespace hdl
 
 extern "C" {
 
@@ -164,9 +122,6 @@ int token_stats(const char* fn, const void* hidden, const void* w_vocab, const i
                 fn, plan.bytes, workspace ? workspace_bytes : static_cast<size_t>(0));
   if (!aligned(workspace, 256))
     return fail(HDL_ERR_INVALID_ARG, "%s: workspace must be 256-byte aligned", fn);
-  if (plan.grid > INT32_MAX)
-    return fail(HDL_ERR_UNSUPPORTED, "%s: problem too large for one launch", fn);
-
   hipStream_t s = static_cast<hipStream_t>(stream);
   char* ws = static_cast<char*>(workspace);
   int32_t* rows = reinterpret_cast<int32_t*>(ws + plan.off_rows);
@@ -176,10 +131,19 @@ int token_stats(const char* fn, const void* hidden, const void* w_vocab, const i
   const int64_t row_bytes = d * esz;
 
   // Launches of at most plan.rows_per_launch rows each (one launch for every
-  // configuration up to 4 GiB of hidden states).
+  // configuration up to 4 GiB of hidden states), all with the call's
+  // vocabulary chunking, so every launch's partials fit the planes.  Checked
+  // for every launch before anything is enqueued.
   for (int64_t r0 = 0; r0 < n_rows; r0 += plan.rows_per_launch) {
     const int64_t n = (n_rows - r0) < plan.rows_per_launch ? (n_rows - r0) : plan.rows_per_launch;
-    const hdl::LmheadPlan lp = hdl::make_plan(n, vocab, d, esz);
+    if (n > plan.n_rows || static_cast<size_t>(plan.n_ch) * static_cast<size_t>(n) > plane ||
+        hdl::plan_launch(plan, n).grid > INT32_MAX)
+      return fail(HDL_ERR_UNSUPPORTED, "%s: a launch of %lld rows does not fit the plan", fn,
+                  static_cast<long long>(n));
+  }
+  for (int64_t r0 = 0; r0 < n_rows; r0 += plan.rows_per_launch) {
+    const int64_t n = (n_rows - r0) < plan.rows_per_launch ? (n_rows - r0) : plan.rows_per_launch;
+    const hdl::LmheadLaunch lp = hdl::plan_launch(plan, n);
     float* logp_c = logp + r0;
     float* lse_c = lse_out ? lse_out + r0 : nullptr;
     float* ent_c = entropy ? entropy + r0 : nullptr;
@@ -194,9 +158,9 @@ int token_stats(const char* fn, const void* hidden, const void* w_vocab, const i
     a.n_scored = n_scored;
     a.d = d;
     a.vocab = vocab;
-    a.n_vt = lp.n_vt;
-    a.tpc = lp.tpc;
-    a.n_ch = lp.n_ch;
+    a.n_vt = plan.n_vt;
+    a.tpc = plan.tpc;
+    a.n_ch = plan.n_ch;
     a.n_grt = lp.n_grt;
     a.part_stride = n;
     a.part_m = part;
@@ -365,7 +329,7 @@ BwdPlan make_bwd_plan(int64_t n_rows, int64_t vocab, int64_t d) {
   p.off_rows = off;
   off = round_up(off + sizeof(int32_t) * static_cast<size_t>(n_rows), 256);
   p.off_count = off;
-  off = round_up(off + sizeof(int32_t) * (64 + static_cast<size_t>((n_rows + 4095) / 4096)), 256);
+  off = round_up(off + sizeof(int32_t) * (64 + static_cast<size_t>(hdl::ceil_div(n_rows, hdl::kCountBlockRows))), 256);
   p.off_g = off;    // G chunk-major [v_pad / 8][nc][8] bf16
   off = round_up(off + 2 * static_cast<size_t>(p.nc) * static_cast<size_t>(p.v_pad), 256);
   p.off_hc = off;   // the chunk's scored hidden rows, gathered chunk-major [nc / 8][d][8] bf16
@@ -452,7 +416,8 @@ int hdl_token_logprobs_backward(const void* hidden, const void* w_vocab, const i
     return fail(HDL_ERR_WORKSPACE, "%s: workspace of %zu bytes needed, %zu given", fn, plan.bytes,
                 workspace ? workspace_bytes : static_cast<size_t>(0));
   if (!aligned(workspace, 256)) return fail(HDL_ERR_INVALID_ARG, "%s: workspace must be 256-byte aligned", fn);
-  if (plan.fwd.grid > INT32_MAX) return fail(HDL_ERR_UNSUPPORTED, "%s: problem too large for one launch", fn);
+  const hdl::LmheadLaunch grad_launch = hdl::plan_launch(plan.fwd, plan.nc);
+  if (grad_launch.grid > INT32_MAX) return fail(HDL_ERR_UNSUPPORTED, "%s: problem too large for one launch", fn);
 
   hipStream_t s = static_cast<hipStream_t>(stream);
   char* ws = static_cast<char*>(workspace);
@@ -491,7 +456,7 @@ int hdl_token_logprobs_backward(const void* hidden, const void* w_vocab, const i
       a.n_vt = plan.fwd.n_vt;
       a.tpc = plan.fwd.tpc;
       a.n_ch = plan.fwd.n_ch;
-      a.n_grt = plan.fwd.n_grt;
+      a.n_grt = grad_launch.n_grt;
       a.row_base = base;
       a.row_cap = plan.nc;
       a.lse_in = lse_b;
@@ -501,7 +466,7 @@ int hdl_token_logprobs_backward(const void* hidden, const void* w_vocab, const i
       a.g_cols = plan.v_pad;
       TimedLaunch tg_;
       if ((e = tg_.start(s)) != hipSuccess) return hip_fail(e, "timing event");
-      if ((e = hdl::launch_lmhead_grad(a, plan.fwd.grid, s)) != hipSuccess)
+      if ((e = hdl::launch_lmhead_grad(a, grad_launch.grid, s)) != hipSuccess)
         return hip_fail(e, "gradient kernel launch");
       if ((e = tg_.stop(HDL_PROFILE_GRAD, s)) != hipSuccess) return hip_fail(e, "timing event");
       // 2. the chunk's scored hidden rows, gathered chunk-major along the row

@@ -6,35 +6,9 @@
 #include <stddef.h>
 #include <stdint.h>
 
+#include "plan.h"
+
 namespace hdl {
-
-// Fused lm-head tile geometry (see lmhead_logprob.hip).
-constexpr int kTileV = 256;         // vocabulary rows per workgroup tile
-constexpr int kTileN = 256;         // token rows per workgroup tile
-constexpr int kGroupRT = 8;         // row tiles per per-XCD launch group
-constexpr int kGroupCH = 32 / kGroupRT; // vocabulary chunks per per-XCD launch group
-constexpr int kNumXcd = 8;          // XCDs per MI355X; workgroups go round-robin
-
-// How one hdl_token_logprobs call is cut into work items.  Every quantity
-// depends on the sizes only, so the workspace size can be computed up front.
-struct LmheadPlan {
-  int64_t n_rows;       // rows per launch (upper bound of scored rows)
-  int64_t rows_per_launch;  // a call is cut into launches of at most this many rows
-  int64_t n_vt;         // vocabulary tiles of kTileV rows
-  int64_t tpc;          // vocabulary tiles per chunk (one work item's span)
-  int64_t n_ch;         // vocabulary chunks
-  int64_t n_rt_max;     // row tiles if every row is scored
-  int64_t n_grt;        // row-tile groups
-  int64_t n_gch;        // chunk groups
-  int64_t grid;         // workgroups launched
-  // workspace layout (byte offsets)
-  size_t off_rows, off_count, off_part, bytes;
-};
-
-// Largest number of rows one launch may cover: every hidden-state byte offset
-// of a launch must fit in 32 bits (the DMA uses a 64-bit base + 32-bit offset).
-int64_t rows_per_launch(int64_t d, int esz);
-LmheadPlan make_plan(int64_t n_rows, int64_t vocab, int64_t d, int esz);
 
 struct LmheadArgs {
   const void* hidden;

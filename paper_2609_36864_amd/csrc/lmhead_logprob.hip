@@ -110,18 +110,9 @@ __global__ __launch_bounds__(kThreads, 1) void lmhead_logprob_kernel(LmheadArgs 
   const int half = lane >> 5;
   const int col = lane & 31;
 
-  // ---- work item: XCD-aware (row tile, vocabulary chunk) ------------------
-  // Workgroups are dealt to the XCDs round-robin.  The j-th workgroup of an
-  // XCD belongs to launch group (j / 32) of that XCD; a group is a block of
-  // kGroupRT row tiles x kGroupCH vocabulary chunks, so the workgroups resident on one XCD
-  // at a time share hidden tiles and W tiles through that XCD's L2.
-  const int64_t b = blockIdx.x;
-  const int64_t xcd = b % kNumXcd;
-  const int64_t j = b / kNumXcd;
-  const int64_t grp = (j / (kGroupRT * kGroupCH)) * kNumXcd + xcd;
-  const int loc = static_cast<int>(j % (kGroupRT * kGroupCH));
-  const int64_t rt = (grp % p.n_grt) * kGroupRT + (loc % kGroupRT);
-  const int64_t ch = (grp / p.n_grt) * kGroupCH + (loc / kGroupRT);
+  // ---- work item: XCD-aware (row tile, vocabulary chunk), see plan.h -----
+  int64_t rt, ch;
+  work_item(blockIdx.x, p.n_grt, &rt, &ch);
   int64_t n_s = *p.n_scored - p.row_base;
   n_s = n_s < 0 ? 0 : (n_s > p.row_cap ? p.row_cap : n_s);
   const int64_t n_rt = (n_s + kTileN - 1) / kTileN;

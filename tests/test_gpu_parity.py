@@ -442,3 +442,75 @@ def test_degenerate_vocabularies_and_large_logits(hdl):
     assert np.all(np.isfinite(lp))
     err = np.abs(lp - want).max()
     assert err <= TOL_BF16, f"max |log p error| {err:.3g} at |lse| up to {np.abs(want_lse).max():.0f}"
+
+
+@pytest.mark.parametrize("n_rows,d", [(8192, 256), (8192, 200), (65536, 256), (65536, 136)])
+def test_work_items_spanning_several_vocab_tiles(hdl, n_rows, d):
+    # The number of vocabulary tiles per work item follows the call's row
+    # count, not its scored rows: 8,192 rows x 513 vocabulary tiles give 2
+    # tiles per item, 65,536 rows give 16.  A sparse mask keeps the oracle's
+    # share small while every scored row runs through items that carry their
+    # DMA pipeline across vocabulary-tile boundaries (and, for d % 64 != 0,
+    # zero-fill the K tail of every tile's last slice); the last chunk is
+    # ragged (513 tiles, the last one with 77 live rows).
+    V = 131072 + 77
+    g = torch.Generator().manual_seed(n_rows + d)
+    W = (torch.randn(V, d, generator=g) * 0.05).to(torch.bfloat16)
+    H = torch.randn(n_rows, d, generator=g).to(torch.bfloat16)
+    y = torch.randint(0, V, (n_rows,), generator=g, dtype=torch.int32)
+    y[::5] = torch.randint(V - 77, V, (len(y[::5]),), generator=g, dtype=torch.int32)   # last tile
+    mask = (torch.rand(n_rows, generator=g) < 300.0 / n_rows).to(torch.uint8)
+    mask[-1] = 1
+    rows = np.nonzero(mask.numpy())[0]
+    lp, lse = run_logprobs(hdl, H, W, y, mask)
+    want, want_lse = oracle_rows(H, W, y, rows)
+    err = np.abs(lp[rows] - want)
+    print(f"n_rows={n_rows} d={d}: {len(rows)} scored rows, max |log p error| {err.max():.3g}")
+    assert err.max() <= TOL_BF16
+    assert np.abs(lse[rows] - want_lse).max() <= TOL_BF16
+    off = np.ones(n_rows, bool)
+    off[rows] = False
+    assert np.all(lp[off] == 0.0)
+    # entropy through the same items
+    Hd, Wd = H.cuda(), W.cuda()
+    _, _, ent = hdl.token_logprobs(Hd, Wd, y.cuda(), mask.cuda(), want_entropy=True)
+    torch.cuda.synchronize()
+    want_ent = O.token_entropy(as_f64(H[torch.as_tensor(rows)]), as_f64(W))
+    assert np.abs(ent.cpu().numpy()[rows] - want_ent).max() <= TOL_BF16
+
+
+def test_remainder_launch_keeps_the_call_chunking(hdl):
+    # bf16, d = 5120, V = 32000: a launch takes at most 419,328 rows (4 GiB of
+    # hidden states), so 446,208 rows run as 419,328 + 26,880.  The remainder
+    # launch uses the call's vocabulary chunking; chunked on its own it would
+    # need 125 chunks x 26,880 rows of partials, more than the workspace's
+    # 8 x 419,328.  Every row of the remainder is scored, so the last chunk's
+    # partials of its last compacted rows are exactly the ones that would not
+    # fit; those rows and rows before the cut are checked against the oracle,
+    # for log p and for the entropy (whose partial plane is the last one).
+    n, d, V = 446208, 5120, 32000
+    cut = 419328
+    gen = torch.Generator(device="cuda").manual_seed(91)
+    H = torch.empty(n, d, device="cuda", dtype=torch.bfloat16)
+    for r0 in range(0, n, 65536):
+        r1 = min(n, r0 + 65536)
+        H[r0:r1] = torch.randn(r1 - r0, d, device="cuda", generator=gen).to(torch.bfloat16)
+    W = (torch.randn(V, d, device="cuda", generator=gen) * 0.02).to(torch.bfloat16)
+    y = torch.randint(0, V, (n,), device="cuda", dtype=torch.int32, generator=gen)
+    m = (torch.rand(n, device="cuda", generator=gen) < 0.01).to(torch.uint8)
+    m[cut:] = 1
+    lp, lse, ent = hdl.token_logprobs(H, W, y, m, want_entropy=True)
+    torch.cuda.synchronize()
+    rng = np.random.default_rng(3)
+    before = np.nonzero(m[:cut].cpu().numpy())[0]
+    rows = np.unique(np.concatenate([rng.choice(before, 40, replace=False),
+                                     np.arange(cut, cut + 8), np.arange(n - 5400, n, 45), [n - 1]]))
+    idx = torch.as_tensor(rows, device="cuda")
+    Hs = as_f64(H[idx].cpu())
+    Wd = as_f64(W.cpu())
+    want, want_lse = O.token_logprobs(Hs, Wd, y[idx].cpu().numpy())
+    err = np.abs(lp[idx].cpu().numpy() - want)
+    print(f"remainder launch: max |log p error| {err.max():.3g} over {len(rows)} rows")
+    assert err.max() <= TOL_BF16
+    assert np.abs(lse[idx].cpu().numpy() - want_lse).max() <= TOL_BF16
+    assert np.abs(ent[idx].cpu().numpy() - O.token_entropy(Hs, Wd)).max() <= TOL_BF16
