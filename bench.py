@@ -6,8 +6,11 @@ in HBM: both contexts' teacher-forced log-probabilities of every eligible
 token through the fused lm-head kernel (hdl_token_logprobs), then the
 divergence score and per-root top-k (hdl_select_branch_points).
 
-Default workload: 8 roots x 2 contexts, T=4096, d=2048, V=151936, bf16, the
-first 32 positions of each root excluded, k=8.
+Default workload (the largest configuration that fits one GPU): the agent
+multi-turn batch, 32 roots x 2 contexts, T=8192, d=4096, V=151936, bf16, with
+seeded tool-observation spans masked out of every root (about 64 % of the
+524,288 rows are scored), k=8.  --workload c2 | c3 | c5 | tiny selects the
+other configurations.
 
 Prints one JSON line:  value = scored tokens/s (both contexts), plus the
 fused kernel's roofline (achieved TFLOP/s of algorithmic 2*d*V flops per
@@ -125,6 +128,19 @@ def mfma_ceiling():
     return json.loads(r.stdout.strip().splitlines()[-1])
 
 
+def host_cores():
+    """(os.cpu_count(), threads of the BLAS pool the float64 oracle's matrix
+    products run on): the oracle's exponentials and sums run on one thread,
+    its products on the BLAS pool."""
+    n = os.cpu_count() or 1
+    try:
+        from threadpoolctl import threadpool_info
+        blas = max([int(i.get("num_threads", 1)) for i in threadpool_info() if i.get("user_api") == "blas"] or [1])
+    except Exception:  # pragma: no cover - informational only
+        blas = n
+    return n, blas
+
+
 def cpu_baseline(w, budget_s: float = 15.0, max_rows: int = 32768, entropy: bool = False):
     """Time the float64 oracle on a seeded sample of eligible rows (both
     contexts; the original context only for the entropy selector) on the host
@@ -132,11 +148,7 @@ def cpu_baseline(w, budget_s: float = 15.0, max_rows: int = 32768, entropy: bool
     import numpy as np
     import torch
     from oracle import hdl_oracle as O
-    try:
-        from threadpoolctl import threadpool_info
-        cores = max([int(i.get("num_threads", 1)) for i in threadpool_info() if i.get("user_api") == "blas"] or [1])
-    except Exception:  # pragma: no cover - informational only
-        cores = os.cpu_count() or 1
+    cores, blas_threads = host_cores()
     c = w.cfg
     if c.dtype == "bf16":
         Wd = O.bf16_bits_to_f64(w.W.view(torch.int16).numpy().view(np.uint16))
@@ -163,7 +175,8 @@ def cpu_baseline(w, budget_s: float = 15.0, max_rows: int = 32768, entropy: bool
             O.token_logprobs(H, Wd, tokens[rows])
         t_total += time.perf_counter() - t0
         done += len(rows)
-    return {"value": done / t_total, "unit": "scored tokens/s", "cores": cores, "kind": "oracle",
+    return {"value": done / t_total, "unit": "scored tokens/s", "cores": blas_threads, "kind": "oracle",
+            "host_cpus": cores, "blas_threads": blas_threads,
             "sample": f"{done} eligible rows drawn from "
                       f"{'the original context' if entropy else 'both contexts'} of this workload "
                       f"(float64 lm-head {'entropy' if entropy else 'log-softmax'}, {t_total:.1f} s)"}
@@ -174,7 +187,8 @@ def main() -> int:
     ap.add_argument("--gpus", type=int, default=1)
     ap.add_argument("--steps", type=int, default=20)
     ap.add_argument("--warmup", type=int, default=3)
-    ap.add_argument("--workload", default="c2", help="tiny | c2 | c3 | c4 | c5 (default c2)")
+    ap.add_argument("--workload", default="c4",
+                    help="tiny | c2 | c3 | c4 | c5 (default c4, the largest single-GPU configuration)")
     ap.add_argument("--selector", default="hdl", choices=["hdl", "entropy"],
                     help="hdl: both contexts, |delta log p| top-k (default); entropy: the Entropy "
                          "baseline, next-token entropy of the original context and its top-k")
@@ -360,11 +374,7 @@ def cpu_baseline_backward(w, budget_s: float = 15.0, max_rows: int = 2048):
     import numpy as np
     import torch
     from oracle import hdl_oracle as O
-    try:
-        from threadpoolctl import threadpool_info
-        cores = max([int(i.get("num_threads", 1)) for i in threadpool_info() if i.get("user_api") == "blas"] or [1])
-    except Exception:  # pragma: no cover - informational only
-        cores = os.cpu_count() or 1
+    cores, blas_threads = host_cores()
     c = w.cfg
     Wd = O.bf16_bits_to_f64(w.W.view(torch.int16).numpy().view(np.uint16))
     n0 = c.R * c.T
@@ -382,7 +392,8 @@ def cpu_baseline_backward(w, budget_s: float = 15.0, max_rows: int = 2048):
         O.token_logprobs_backward(H, Wd, tokens[rows], g)
         t_total += time.perf_counter() - t0
         done += len(rows)
-    return {"value": done / t_total, "unit": "trained tokens/s", "cores": cores, "kind": "oracle",
+    return {"value": done / t_total, "unit": "trained tokens/s", "cores": blas_threads, "kind": "oracle",
+            "host_cpus": cores, "blas_threads": blas_threads,
             "sample": f"{done} eligible original-context rows of this workload (float64 logits, "
                       f"softmax gradient, dL/dh and dL/dW, {t_total:.1f} s)"}
 
