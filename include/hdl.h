@@ -122,6 +122,32 @@ int hdl_token_logprobs_entropy(const void* hidden, const void* w_vocab, const in
                                void* workspace, size_t workspace_bytes, void* stream);
 
 /*
+ * hdl_token_logprobs without a workspace argument, for callers that cannot
+ * allocate device memory: code under HIP graph capture, tight serving loops,
+ * harnesses that forbid hipMalloc.  The library allocates nothing for it
+ * either: its workspace is a fixed 32 MiB device array inside the library
+ * (one per GPU, held until the process ends; its address is looked up once
+ * per device on the first call on that device, with that device current).
+ *
+ * Arguments, outputs, numerics and error behaviour are those of
+ * hdl_token_logprobs (without the entropy).  The caller still provides every
+ * input and output buffer.  Where the default vocabulary chunking's partials
+ * do not fit the array, the call uses fewer, longer chunks, so results may
+ * differ from hdl_token_logprobs by rounding (the same bound holds); where
+ * they fit, the results are bit-identical.  A launch (at most 4 GiB of hidden
+ * states) needs 16 bytes of the array per row: a call whose launch would
+ * cover more than about 2.09 million rows (only possible for d * element
+ * size below 2 KiB) returns HDL_ERR_UNSUPPORTED before touching the GPU.
+ *
+ * Every call on one GPU uses that GPU's array and leaves its contents
+ * behind; nothing in it has to start at zero.  Calls that overlap on one GPU
+ * (concurrent streams or threads) race on the array: serialise them.
+ */
+int hdl_token_logprobs_noalloc(const void* hidden, const void* w_vocab, const int32_t* tokens,
+                               const uint8_t* mask, int64_t n_rows, int64_t d, int64_t vocab,
+                               int dtype, float* logp, float* lse_out, void* stream);
+
+/*
  * Hindsight-divergence score and per-root branch-point selection (Eq. 2 and
  * the ranking of Sec. 3.2):
  *

@@ -19,7 +19,7 @@ from typing import Optional, Tuple
 import torch
 
 __all__ = ["HdlError", "HDL_F32", "HDL_BF16", "HDL_MAX_K", "library_path", "load_library",
-           "workspace_size", "token_logprobs", "token_logprobs_backward", "select_branch_points",
+           "workspace_size", "token_logprobs", "token_logprobs_noalloc", "token_logprobs_backward", "select_branch_points",
            "select_top_k", "select_constrained", "allocate_continuations", "group_advantages",
            "policy_loss_grad", "rescore",
            "profile_enable", "profile_read", "abi_version"]
@@ -60,6 +60,9 @@ def load_library() -> ctypes.CDLL:
     L.hdl_token_logprobs_entropy.argtypes = [c_vp, c_vp, c_vp, c_vp, c_i64, c_i64, c_i64, ctypes.c_int,
                                              c_vp, c_vp, c_vp, c_vp, c_sz, c_vp]
     L.hdl_token_logprobs_entropy.restype = ctypes.c_int
+    L.hdl_token_logprobs_noalloc.argtypes = [c_vp, c_vp, c_vp, c_vp, c_i64, c_i64, c_i64, ctypes.c_int,
+                                             c_vp, c_vp, c_vp]
+    L.hdl_token_logprobs_noalloc.restype = ctypes.c_int
     L.hdl_select_top_k.argtypes = [c_vp, c_vp, c_i64, c_i64, ctypes.c_int32, c_vp, c_vp, c_vp, c_vp]
     L.hdl_select_top_k.restype = ctypes.c_int
     L.hdl_token_logprobs_backward_workspace_size.argtypes = [c_i64, c_i64, c_i64, ctypes.c_int]
@@ -428,6 +431,37 @@ def policy_loss_grad(adv: torch.Tensor, traj: torch.Tensor, logp_new: torch.Tens
                                   float(eps_high), float(scale), grad.data_ptr(), loss.data_ptr(),
                                   _stream_handle(traj.device)))
     return grad, loss
+
+
+@_on_tensor_device
+def token_logprobs_noalloc(hidden: torch.Tensor, w_vocab: torch.Tensor, tokens: torch.Tensor,
+                           mask: Optional[torch.Tensor], logp: torch.Tensor,
+                           lse: Optional[torch.Tensor] = None) -> None:
+    """hdl_token_logprobs_noalloc: log p (and lse) into caller-given outputs,
+    with the library's fixed device scratch instead of a workspace; nothing
+    is allocated (usable under graph capture).  Calls on one GPU must not
+    overlap.  Arguments as for token_logprobs; logp and lse are fp32 [n_rows]."""
+    L = load_library()
+    for name, t in (("hidden", hidden), ("w_vocab", w_vocab), ("tokens", tokens), ("logp", logp)):
+        _require_cuda(name, t)
+    n_rows, d = hidden.shape
+    if hidden.dtype != w_vocab.dtype or hidden.dtype not in (torch.bfloat16, torch.float32):
+        raise ValueError("hidden and w_vocab must both be bfloat16 or both float32")
+    if tokens.dtype != torch.int32 or tokens.shape != (n_rows,):
+        raise ValueError("tokens must be int32 [n_rows]")
+    for name, t in (("logp", logp), ("lse", lse)):
+        if t is not None and (t.dtype != torch.float32 or t.shape != (n_rows,)):
+            raise ValueError(f"{name} must be float32 [n_rows]")
+    if mask is not None:
+        _require_cuda("mask", mask)
+        if mask.dtype == torch.bool:
+            mask = mask.view(torch.uint8)
+        if mask.dtype != torch.uint8 or mask.shape != (n_rows,):
+            raise ValueError("mask must be uint8 [n_rows]")
+    dt = HDL_BF16 if hidden.dtype == torch.bfloat16 else HDL_F32
+    _check(L.hdl_token_logprobs_noalloc(hidden.data_ptr(), w_vocab.data_ptr(), tokens.data_ptr(), _ptr(mask),
+                                        n_rows, d, w_vocab.shape[0], dt, logp.data_ptr(), _ptr(lse),
+                                        _stream_handle(hidden.device)))
 
 
 def rescore(hidden_both: torch.Tensor, w_vocab: torch.Tensor, tokens: torch.Tensor,

@@ -12,6 +12,20 @@
 #include "../../include/hdl.h"
 #include "hdl_internal.h"
 
+// ---- the allocation-free entry point's scratch ---------------------------
+// A fixed device array holds hdl_token_logprobs_noalloc's workspace (the
+// compacted row list, the scored-row count and the chunk partials), so that
+// callers that cannot allocate (code under graph capture, serving loops)
+// still get the fused path.  Every GPU the library runs on holds its own
+// copy until the process ends.  Its host-side name is not a device address:
+// the address is taken once per device with hipGetSymbolAddress and only
+// that address is passed to kernels.  Nothing in it needs clearing between
+// calls: every call writes each element it reads first.  Calls that overlap
+// on one GPU (different streams or threads) share it and race.
+
+constexpr size_t kScratchBytes = size_t{32} << 20;
+static __device__ __align__(256) unsigned char scratch[kScratchBytes];
+
 namespace {
 
 thread_local char g_last_error[512] = "";
@@ -94,12 +108,10 @@ size_t hdl_token_logprobs_workspace_size(int64_t n_rows, int64_t d, int64_t voca
 
 namespace {
 
-// Shared implementation of hdl_token_logprobs / hdl_token_logprobs_entropy.
-int token_stats(const char* fn, const void* hidden, const void* w_vocab, const int32_t* tokens,
-                const uint8_t* mask, int64_t n_rows, int64_t d, int64_t vocab, int dtype, float* logp,
-                float* lse_out, float* entropy, void* workspace, size_t workspace_bytes,
-                void* stream) {
-  g_last_error[0] = '\0';
+// Argument checks shared by the log-probability entry points; on success
+// *esz is the element size.  Nothing is launched.
+int check_stats_args(const char* fn, const void* hidden, const void* w_vocab, const int32_t* tokens,
+                     float* logp, int64_t n_rows, int64_t d, int64_t vocab, int dtype, int* esz) {
   if (!hidden || !w_vocab || !tokens || !logp)
     return fail(HDL_ERR_INVALID_ARG, "%s: null hidden, w_vocab, tokens or logp", fn);
   if (n_rows <= 0 || d <= 0 || vocab <= 0)
@@ -113,22 +125,27 @@ int token_stats(const char* fn, const void* hidden, const void* w_vocab, const i
     return fail(HDL_ERR_UNSUPPORTED, "%s: d=%lld is not a multiple of 8", fn, static_cast<long long>(d));
   if (!aligned(hidden, 16) || !aligned(w_vocab, 16))
     return fail(HDL_ERR_INVALID_ARG, "%s: hidden and w_vocab must be 16-byte aligned", fn);
-  const int esz = dtype == HDL_BF16 ? 2 : 4;
-  if (hdl::rows_per_launch(d, esz) < hdl::kTileN)
+  *esz = dtype == HDL_BF16 ? 2 : 4;
+  if (hdl::rows_per_launch(d, *esz) < hdl::kTileN)
     return fail(HDL_ERR_UNSUPPORTED, "%s: hidden rows larger than 16 MiB", fn);
-  const hdl::LmheadPlan plan = hdl::make_plan(n_rows, vocab, d, esz);
-  if (!workspace || workspace_bytes < plan.bytes)
-    return fail(HDL_ERR_WORKSPACE, "%s: workspace of %zu bytes needed, %zu given",
-                fn, plan.bytes, workspace ? workspace_bytes : static_cast<size_t>(0));
-  if (!aligned(workspace, 256))
-    return fail(HDL_ERR_INVALID_ARG, "%s: workspace must be 256-byte aligned", fn);
+  return HDL_OK;
+}
+
+// Shared implementation of the log-probability entry points: compaction,
+// fused kernel and merge for each launch of the call, in the workspace `ws`
+// laid out by `plan`.  `timed`: bracket the fused kernel with the timing
+// hook's events when it is on.
+int token_stats(const char* fn, const void* hidden, const void* w_vocab, const int32_t* tokens,
+                const uint8_t* mask, int64_t n_rows, int64_t d, int64_t vocab, int esz, int dtype,
+                float* logp, float* lse_out, float* entropy, const hdl::LmheadPlan& plan, char* ws,
+                bool timed, void* stream) {
   hipStream_t s = static_cast<hipStream_t>(stream);
-  char* ws = static_cast<char*>(workspace);
   int32_t* rows = reinterpret_cast<int32_t*>(ws + plan.off_rows);
   int32_t* n_scored = reinterpret_cast<int32_t*>(ws + plan.off_count);
   float* part = reinterpret_cast<float*>(ws + plan.off_part);
   const size_t plane = static_cast<size_t>(plan.n_ch) * static_cast<size_t>(plan.n_rows);
   const int64_t row_bytes = d * esz;
+  if (entropy && plan.planes < 4) return fail(HDL_ERR_UNSUPPORTED, "%s: no entropy plane in the plan", fn);
 
   // Launches of at most plan.rows_per_launch rows each (one launch for every
   // configuration up to 4 GiB of hidden states), all with the call's
@@ -171,13 +188,52 @@ int token_stats(const char* fn, const void* hidden, const void* w_vocab, const i
     a.row_cap = n;
 
     TimedLaunch tl;
-    if ((e = tl.start(s)) != hipSuccess) return hip_fail(e, "timing event");
+    if (timed && (e = tl.start(s)) != hipSuccess) return hip_fail(e, "timing event");
     e = hdl::launch_lmhead(a, lp.grid, dtype == HDL_BF16, s);
     if (e != hipSuccess) return hip_fail(e, "lm-head kernel launch");
     if ((e = tl.stop(HDL_PROFILE_LMHEAD, s)) != hipSuccess) return hip_fail(e, "timing event");
     e = hdl::launch_merge(a, n, logp_c, lse_c, ent_c, s);
     if (e != hipSuccess) return hip_fail(e, "merge kernel launch");
   }
+  return HDL_OK;
+}
+
+// The workspace entry points: the caller's workspace, the default plan.
+int token_stats_ws(const char* fn, const void* hidden, const void* w_vocab, const int32_t* tokens,
+                   const uint8_t* mask, int64_t n_rows, int64_t d, int64_t vocab, int dtype, float* logp,
+                   float* lse_out, float* entropy, void* workspace, size_t workspace_bytes, void* stream) {
+  g_last_error[0] = '\0';
+  int esz = 0;
+  int st = check_stats_args(fn, hidden, w_vocab, tokens, logp, n_rows, d, vocab, dtype, &esz);
+  if (st != HDL_OK) return st;
+  const hdl::LmheadPlan plan = hdl::make_plan(n_rows, vocab, d, esz);
+  if (!workspace || workspace_bytes < plan.bytes)
+    return fail(HDL_ERR_WORKSPACE, "%s: workspace of %zu bytes needed, %zu given",
+                fn, plan.bytes, workspace ? workspace_bytes : static_cast<size_t>(0));
+  if (!aligned(workspace, 256))
+    return fail(HDL_ERR_INVALID_ARG, "%s: workspace must be 256-byte aligned", fn);
+  return token_stats(fn, hidden, w_vocab, tokens, mask, n_rows, d, vocab, esz, dtype, logp, lse_out, entropy,
+                     plan, static_cast<char*>(workspace), true, stream);
+}
+
+constexpr int kMaxDevices = 64;
+std::mutex g_scratch_mu;
+char* g_scratch_ptr[kMaxDevices] = {};
+
+int scratch_on_current_device(const char* fn, char** out) {
+  int dev = -1;
+  hipError_t e = hipGetDevice(&dev);
+  if (e != hipSuccess) return hip_fail(e, "hipGetDevice");
+  if (dev < 0 || dev >= kMaxDevices) return fail(HDL_ERR_UNSUPPORTED, "%s: device %d", fn, dev);
+  std::lock_guard<std::mutex> lk(g_scratch_mu);
+  if (!g_scratch_ptr[dev]) {
+    void* p = nullptr;
+    e = hipGetSymbolAddress(&p, HIP_SYMBOL(scratch));
+    if (e != hipSuccess) return hip_fail(e, "hipGetSymbolAddress(scratch)");
+    if (!p || !aligned(p, 256)) return fail(HDL_ERR_HIP, "%s: scratch address %p", fn, p);
+    g_scratch_ptr[dev] = static_cast<char*>(p);
+  }
+  *out = g_scratch_ptr[dev];
   return HDL_OK;
 }
 
@@ -189,8 +245,8 @@ int hdl_token_logprobs(const void* hidden, const void* w_vocab, const int32_t* t
                        const uint8_t* mask, int64_t n_rows, int64_t d, int64_t vocab, int dtype,
                        float* logp, float* lse_out, void* workspace, size_t workspace_bytes,
                        void* stream) {
-  return token_stats("hdl_token_logprobs", hidden, w_vocab, tokens, mask, n_rows, d, vocab, dtype,
-                     logp, lse_out, nullptr, workspace, workspace_bytes, stream);
+  return token_stats_ws("hdl_token_logprobs", hidden, w_vocab, tokens, mask, n_rows, d, vocab, dtype,
+                        logp, lse_out, nullptr, workspace, workspace_bytes, stream);
 }
 
 int hdl_token_logprobs_entropy(const void* hidden, const void* w_vocab, const int32_t* tokens,
@@ -201,8 +257,29 @@ int hdl_token_logprobs_entropy(const void* hidden, const void* w_vocab, const in
     g_last_error[0] = '\0';
     return fail(HDL_ERR_INVALID_ARG, "hdl_token_logprobs_entropy: null entropy");
   }
-  return token_stats("hdl_token_logprobs_entropy", hidden, w_vocab, tokens, mask, n_rows, d, vocab,
-                     dtype, logp, lse_out, entropy, workspace, workspace_bytes, stream);
+  return token_stats_ws("hdl_token_logprobs_entropy", hidden, w_vocab, tokens, mask, n_rows, d, vocab,
+                        dtype, logp, lse_out, entropy, workspace, workspace_bytes, stream);
+}
+
+int hdl_token_logprobs_noalloc(const void* hidden, const void* w_vocab, const int32_t* tokens,
+                               const uint8_t* mask, int64_t n_rows, int64_t d, int64_t vocab, int dtype,
+                               float* logp, float* lse_out, void* stream) {
+  const char* fn = "hdl_token_logprobs_noalloc";
+  g_last_error[0] = '\0';
+  int esz = 0;
+  int st = check_stats_args(fn, hidden, w_vocab, tokens, logp, n_rows, d, vocab, dtype, &esz);
+  if (st != HDL_OK) return st;
+  hdl::LmheadPlan plan{};
+  if (!hdl::make_plan_bounded(n_rows, vocab, d, esz, 3, kScratchBytes, &plan))
+    return fail(HDL_ERR_UNSUPPORTED,
+                "%s: a launch of %lld rows needs more than the library's fixed %zu-byte scratch "
+                "(16 bytes per row of a launch: at most about %zu rows)",
+                fn, static_cast<long long>(n_rows < hdl::rows_per_launch(d, esz) ? n_rows : hdl::rows_per_launch(d, esz)),
+                kScratchBytes, (kScratchBytes - 4096) / 16);
+  char* ws = nullptr;
+  if ((st = scratch_on_current_device(fn, &ws)) != HDL_OK) return st;
+  return token_stats(fn, hidden, w_vocab, tokens, mask, n_rows, d, vocab, esz, dtype, logp, lse_out, nullptr,
+                     plan, ws, false, stream);
 }
 
 int hdl_select_branch_points(const float* logp_orig, const float* logp_hind, const uint8_t* mask,

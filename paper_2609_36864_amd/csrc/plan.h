@@ -97,8 +97,9 @@ inline LmheadPlan make_plan(int64_t n_rows_total, int64_t vocab, int64_t d, int 
 }
 
 // The plan of a call whose whole workspace must fit in `total_bytes`, with
-// `planes` partial planes: the default chunking where it fits, else fewer,
-// longer chunks.  Returns false when not even one chunk fits.
+// `planes` partial planes: the default chunking where it fits (then the
+// results equal those of the default plan bit for bit), else fewer, longer
+// chunks.  Returns false when not even one chunk fits.
 inline bool make_plan_bounded(int64_t n_rows_total, int64_t vocab, int64_t d, int esz, int planes,
                               size_t total_bytes, LmheadPlan* out) {
   LmheadPlan p{};
@@ -113,10 +114,9 @@ inline bool make_plan_bounded(int64_t n_rows_total, int64_t vocab, int64_t d, in
   const size_t per_chunk = sizeof(float) * static_cast<size_t>(planes) * static_cast<size_t>(rows);
   if (total_bytes < fixed + per_chunk) return false;
   const int64_t n_ch_fit = static_cast<int64_t>((total_bytes - fixed) / per_chunk);
-  const int64_t n_ch_default = ceil_div(p.n_vt, default_tpc(rows, p.n_vt));
-  const int64_t n_ch = n_ch_default < n_ch_fit ? n_ch_default : n_ch_fit;
-  p.tpc = ceil_div(p.n_vt, n_ch);
-  p.n_ch = ceil_div(p.n_vt, p.tpc);   // <= n_ch
+  p.tpc = default_tpc(rows, p.n_vt);
+  if (ceil_div(p.n_vt, p.tpc) > n_ch_fit) p.tpc = ceil_div(p.n_vt, n_ch_fit);   // fewer, longer chunks
+  p.n_ch = ceil_div(p.n_vt, p.tpc);   // <= n_ch_fit
   layout_workspace(p, rows, planes);
   if (p.bytes > total_bytes) return false;
   *out = p;

@@ -89,6 +89,10 @@ static void check_bounded(int64_t n_rows, int64_t d, int64_t vocab, int esz, siz
   CHECK(p.tpc * p.n_ch >= p.n_vt && (p.n_ch - 1) * p.tpc < p.n_vt, "bounded chunking");
   const LmheadPlan def = make_plan(n_rows, vocab, d, esz);
   CHECK(p.n_ch <= def.n_ch, "bounded plan has more chunks than the default");
+  // where the default chunking fits, the bounded plan keeps it
+  LmheadPlan def3 = def;
+  layout_workspace(def3, def.n_rows, 3);
+  if (def3.bytes <= total) CHECK(p.tpc == def.tpc && p.n_ch == def.n_ch, "bounded plan changed a chunking that fits");
   const size_t plane = static_cast<size_t>(p.n_ch) * static_cast<size_t>(p.n_rows);
   for (int64_t r0 = 0; r0 < n_rows; r0 += p.rows_per_launch) {
     const int64_t n = n_rows - r0 < p.rows_per_launch ? n_rows - r0 : p.rows_per_launch;

@@ -169,3 +169,15 @@ def test_binding_rejects_host_tensors_before_any_launch():
         hdl.select_top_k(torch.zeros(2, 8), None, 2)
     with pytest.raises(ValueError):
         hdl.group_advantages(torch.zeros(2, 4))
+
+
+def test_noalloc_argument_checks_before_any_hip_call(lib):
+    f = lib.hdl_token_logprobs_noalloc
+    p = 0x1000   # never dereferenced: every call below fails its checks first
+    assert f(None, p, p, None, 10, 64, 100, 1, p, None, None) == -1
+    assert f(p, p, p, None, 0, 64, 100, 1, p, None, None) == -1
+    assert f(p, p, p, None, 10, 60, 100, 1, p, None, None) == -2
+    assert f(p, p, p, None, 10, 64, 100, 9, p, None, None) == -2
+    # 3 million rows of d = 8 would need 48 MB of the library's 32 MiB array
+    assert f(p, p, p, None, 3_000_000, 8, 1000, 1, p, None, None) == -2
+    assert b"scratch" in lib.hdl_last_error()
