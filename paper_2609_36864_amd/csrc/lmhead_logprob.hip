@@ -77,6 +77,40 @@ __device__ __forceinline__ void combine(float& m, float& s, float& z, float& t, 
   z = fmaxf(z, z2);
 }
 
+// The MFMA shape of this kernel: v_mfma_f32_16x16x32_bf16 (fp32 inputs: four
+// v_mfma_f32_16x16x4_f32 over one 16-byte fragment).  A fragment is 16 rows
+// of one operand: lane l holds row (l mod 16) and the 16-byte chunk
+// (4 ks + l div 16) of the K-slice, i.e. 8 bf16 (4 fp32) consecutive K
+// values; A and B fragments take the same K positions, so the contraction is
+// exact whatever order the hardware sums them in.  The 16 x 16 fp32 result
+// block sits in 4 registers per lane: column (l mod 16), rows
+// 4 (l div 16) + i.
+template <bool BF16> struct Mma16;
+
+template <> struct Mma16<true> {
+  __device__ __forceinline__ static void run(const uint4& a, const uint4& b, f32x4_t& c) {
+    c = __builtin_amdgcn_mfma_f32_16x16x32_bf16(__builtin_bit_cast(bf16x8_t, a), __builtin_bit_cast(bf16x8_t, b), c,
+                                                0, 0, 0);
+  }
+};
+
+template <> struct Mma16<false> {
+  // Four K = 4 steps; lane group g supplies K offset 4 g + j in step j, the
+  // same for both operands, so the four steps cover the fragment's 16 K values.
+  __device__ __forceinline__ static void run(const uint4& a, const uint4& b, f32x4_t& c) {
+    c = __builtin_amdgcn_mfma_f32_16x16x4f32(__uint_as_float(a.x), __uint_as_float(b.x), c, 0, 0, 0);
+    c = __builtin_amdgcn_mfma_f32_16x16x4f32(__uint_as_float(a.y), __uint_as_float(b.y), c, 0, 0, 0);
+    c = __builtin_amdgcn_mfma_f32_16x16x4f32(__uint_as_float(a.z), __uint_as_float(b.z), c, 0, 0, 0);
+    c = __builtin_amdgcn_mfma_f32_16x16x4f32(__uint_as_float(a.w), __uint_as_float(b.w), c, 0, 0, 0);
+  }
+};
+
+constexpr int kVB = 8;    // 16-row vocabulary blocks per wave (128 vocabulary rows)
+constexpr int kTB = 4;    // 16-token blocks per wave (kWaveN = 64 tokens)
+constexpr int kKSteps = kChunks / 4;   // K-steps of 4 chunks (64 bytes per row) per K-slice
+static_assert(kTB * 16 == kWaveN, "wave token span");
+static_assert(kKSteps == 2, "a K-slice is two K-steps");
+
 // KTAIL: d is not a multiple of the K-slice, so the last slice of every
 // row needs zero-filling (a separate instantiation keeps that work out of the
 // common case).  EPI selects what each V-tile's logits feed:
@@ -96,9 +130,10 @@ template <bool BF16, bool KTAIL, int EPI>
 __global__ __launch_bounds__(kThreads, 1) void lmhead_logprob_kernel(LmheadArgs p) {
   constexpr bool ENT = EPI == kEpiEntropy;
   constexpr bool GRAD = EPI == kEpiGrad;
-  using M = Mma<BF16>;
+  using M = Mma16<BF16>;
   constexpr int kEsz = BF16 ? 2 : 4;
-  constexpr int kSliceK = M::kElemsPer16B * kChunks;   // K elements per slice
+  constexpr int kElemsPer16B = 16 / kEsz;
+  constexpr int kSliceK = kElemsPer16B * kChunks;   // K elements per slice
 
   __shared__ uint4 lds[kStages][2][kSlots];   // [stage][0 = W, 1 = hidden] = 128 KB
 
@@ -107,8 +142,8 @@ __global__ __launch_bounds__(kThreads, 1) void lmhead_logprob_kernel(LmheadArgs 
   const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);   // wave-uniform
   const int wm = wave & 1;      // which 128 vocabulary rows of the tile
   const int wn = wave >> 1;     // which kWaveN token rows of the tile
-  const int half = lane >> 5;
-  const int col = lane & 31;
+  const int r16 = lane & 15;    // row of a 16-row fragment / column of a result block
+  const int grp = lane >> 4;    // lane group: K chunk of a fragment, row quad of a result block
 
   // ---- work item: XCD-aware (row tile, vocabulary chunk), see plan.h -----
   int64_t rt, ch;
@@ -130,11 +165,11 @@ __global__ __launch_bounds__(kThreads, 1) void lmhead_logprob_kernel(LmheadArgs 
   const char* __restrict__ hbase = static_cast<const char*>(p.hidden);
 
   // ---- this lane's token columns and their sampled tokens ------------------
-  int tok[kNB];
-  float g_lse[kNB], g_up[kNB];   // gradient mode: lse * log2(e) and upstream gradient
+  int tok[kTB];
+  float g_lse[kTB], g_up[kTB];   // gradient mode: lse * log2(e) and upstream gradient
 #pragma unroll
-  for (int bn = 0; bn < kNB; ++bn) {
-    int64_t e = rt * kTileN + wn * kWaveN + bn * 32 + col;
+  for (int bn = 0; bn < kTB; ++bn) {
+    int64_t e = rt * kTileN + wn * kWaveN + bn * 16 + r16;
     e = e < n_s ? e : n_s - 1;
     const int row = p.rows[e];
     tok[bn] = p.tokens[row];
@@ -146,17 +181,17 @@ __global__ __launch_bounds__(kThreads, 1) void lmhead_logprob_kernel(LmheadArgs 
     }
   }
 
-  float run_m[kNB], run_s[kNB], run_z[kNB], run_t[kNB];
+  float run_m[kTB], run_s[kTB], run_z[kTB], run_t[kTB];
 #pragma unroll
-  for (int bn = 0; bn < kNB; ++bn) { run_m[bn] = kNegInf; run_s[bn] = 0.f; run_z[bn] = kNegInf; run_t[bn] = 0.f; }
+  for (int bn = 0; bn < kTB; ++bn) { run_m[bn] = kNegInf; run_s[bn] = 0.f; run_z[bn] = kNegInf; run_t[bn] = 0.f; }
 
-  f32x16_t acc[4][kNB];
+  f32x4_t acc[kVB][kTB];
 #pragma unroll
-  for (int bm = 0; bm < 4; ++bm)
+  for (int bm = 0; bm < kVB; ++bm)
 #pragma unroll
-    for (int bn = 0; bn < kNB; ++bn)
+    for (int bn = 0; bn < kTB; ++bn)
 #pragma unroll
-      for (int q = 0; q < 16; ++q) acc[bm][bn][q] = 0.f;
+      for (int q = 0; q < 4; ++q) acc[bm][bn][q] = 0.f;
 
   // ---- direct global -> LDS loads -----------------------------------------
   // A K-slice of one operand tile is made of 1 KB blocks of kBlockRows rows.
@@ -172,7 +207,8 @@ __global__ __launch_bounds__(kThreads, 1) void lmhead_logprob_kernel(LmheadArgs 
   constexpr bool k_tail = KTAIL;
   const int64_t row_bytes = d * kEsz;
   // Per-lane byte offsets (row start + 16-byte chunk) of this wave's DMA
-  // blocks; a call never spans more than 4 GiB of either operand.
+  // blocks; a launch never spans more than 4 GiB of hidden states, and W is
+  // addressed from the current V-tile's first row.
   uint32_t hoff[kBlocksPerWave];
 #pragma unroll
   for (int i = 0; i < kBlocksPerWave; ++i) {
@@ -245,18 +281,34 @@ __global__ __launch_bounds__(kThreads, 1) void lmhead_logprob_kernel(LmheadArgs 
     for (int sidx = tid; sidx < kSlots; sidx += kThreads) {
       const int row = sidx / kChunks;
       const int chunk = (sidx % kChunks) ^ row_xor(row);
-      if (static_cast<int64_t>(kt) * kSliceK + chunk * M::kElemsPer16B >= d) {
+      if (static_cast<int64_t>(kt) * kSliceK + chunk * kElemsPer16B >= d) {
         lds[stage][0][sidx] = make_uint4(0, 0, 0, 0);
         lds[stage][1][sidx] = make_uint4(0, 0, 0, 0);
       }
     }
   };
-  auto load_frags = [&](int slice, int kk, uint4 (&fa)[4], uint4 (&fb)[kNB]) {
-    const int stage = slice % kStages;
+
+  // ---- fragment reads ------------------------------------------------------
+  // Fragments start at multiples of 16 rows, so a fragment row's swizzle is
+  // that of (lane mod 16): one per-lane offset per K-step, plus immediates.
+  const int frag_lane[kKSteps] = {(r16 * kChunks + ((0 + grp) ^ row_xor(r16))),
+                                  (r16 * kChunks + ((4 + grp) ^ row_xor(r16)))};
+  // the two W fragments (vocabulary blocks 2 pr, 2 pr + 1) of quarter pr of K-step ks
+  auto load_a = [&](int slice, int ks, int pr, uint4 (&dst)[2]) {
+    const uint4* base = &lds[slice % kStages][0][frag_lane[ks]];
 #pragma unroll
-    for (int bm = 0; bm < 4; ++bm) fa[bm] = lds[stage][0][swz(wm * 128 + bm * 32 + col, kk * 2 + half)];
+    for (int j = 0; j < 2; ++j) dst[j] = base[(wm * 128 + (2 * pr + j) * 16) * kChunks];
+  };
+  // hidden-state fragment of token block bn, K-step ks
+  auto load_b = [&](int slice, int ks, int bn, uint4& dst) {
+    dst = lds[slice % kStages][1][frag_lane[ks] + (wn * kWaveN + bn * 16) * kChunks];
+  };
+  // the 2 x kTB MFMAs of quarter pr
+  auto quarter_mfma = [&](const uint4 (&a)[2], const uint4 (&b)[kTB], int pr) {
 #pragma unroll
-    for (int bn = 0; bn < kNB; ++bn) fb[bn] = lds[stage][1][swz(wn * kWaveN + bn * 32 + col, kk * 2 + half)];
+    for (int j = 0; j < 2; ++j)
+#pragma unroll
+      for (int bn = 0; bn < kTB; ++bn) M::run(a[j], b[bn], acc[2 * pr + j][bn]);
   };
 
   // Online max / sum-of-exp update of one V-tile, then capture of the
@@ -265,38 +317,41 @@ __global__ __launch_bounds__(kThreads, 1) void lmhead_logprob_kernel(LmheadArgs 
   auto epilogue = [&](int64_t vt, auto masked_tag) {
     constexpr bool kMasked = decltype(masked_tag)::value;
     const int64_t vbase = vt * kTileV + wm * 128;   // first vocab row of this wave
+    const int64_t vlane = vbase + 4 * grp;          // + 16 bm + i: this lane's rows
 #pragma unroll
-    for (int bn = 0; bn < kNB; ++bn) {
+    for (int bn = 0; bn < kTB; ++bn) {
       if (kMasked) {
 #pragma unroll
-        for (int bm = 0; bm < 4; ++bm)
+        for (int bm = 0; bm < kVB; ++bm)
 #pragma unroll
-          for (int q = 0; q < 16; ++q)
-            if (vbase + bm * 32 + acc_row(q, half) >= V) acc[bm][bn][q] = kNegInf;
+          for (int q = 0; q < 4; ++q)
+            if (vlane + bm * 16 + q >= V) acc[bm][bn][q] = kNegInf;
       }
       float mx = acc[0][bn][0];
 #pragma unroll
-      for (int bm = 0; bm < 4; ++bm)
+      for (int bm = 0; bm < kVB; ++bm)
 #pragma unroll
-        for (int q = 0; q < 16; ++q) mx = fmaxf(mx, acc[bm][bn][q]);
+        for (int q = 0; q < 4; ++q) mx = fmaxf(mx, acc[bm][bn][q]);
       const float mnew = fmaxf(run_m[bn], mx);
       if (!kMasked || mnew != kNegInf) {
         const float mb = mnew * kLog2e;
         float s4[4], t4[4];
 #pragma unroll
-        for (int bm = 0; bm < 4; ++bm) {
+        for (int g4 = 0; g4 < 4; ++g4) {
           float sacc = 0.f, tacc = 0.f;
 #pragma unroll
-          for (int q = 0; q < 16; ++q) {
-            const float zq = acc[bm][bn][q];
-            const float zl = __builtin_fmaf(zq, kLog2e, -mb);   // (z - m) log2(e)
-            const float e = fast_exp2(zl);
-            sacc += e;
-            // (masked rows hold -inf and e = 0; their product term is 0)
-            if (ENT) tacc = __builtin_fmaf(e, (kMasked && zq == kNegInf) ? 0.f : zl, tacc);
-          }
-          s4[bm] = sacc;
-          t4[bm] = tacc;
+          for (int bm = 2 * g4; bm < 2 * g4 + 2; ++bm)
+#pragma unroll
+            for (int q = 0; q < 4; ++q) {
+              const float zq = acc[bm][bn][q];
+              const float zl = __builtin_fmaf(zq, kLog2e, -mb);   // (z - m) log2(e)
+              const float e = fast_exp2(zl);
+              sacc += e;
+              // (masked rows hold -inf and e = 0; their product term is 0)
+              if (ENT) tacc = __builtin_fmaf(e, (kMasked && zq == kNegInf) ? 0.f : zl, tacc);
+            }
+          s4[g4] = sacc;
+          t4[g4] = tacc;
         }
         const float tile_sum = (s4[0] + s4[1]) + (s4[2] + s4[3]);
         const float rescale = fast_exp2(__builtin_fmaf(run_m[bn], kLog2e, -mb));
@@ -306,162 +361,168 @@ __global__ __launch_bounds__(kThreads, 1) void lmhead_logprob_kernel(LmheadArgs 
         run_m[bn] = mnew;
       }
       const int64_t o = static_cast<int64_t>(tok[bn]) - vbase;
-      if (o >= 0 && o < 128) {
-        const int r = static_cast<int>(o) & 31;
-        if (((r >> 2) & 1) == half) {
-          const int code = (static_cast<int>(o) >> 5) * 16 + (r >> 3) * 4 + (r & 3);
-          float zc = kNegInf;
+      if (o >= 0 && o < 128 && ((static_cast<int>(o) >> 2) & 3) == grp) {
+        const int code = (static_cast<int>(o) >> 4) * 4 + (static_cast<int>(o) & 3);   // 4 bm + i
+        float zc = kNegInf;
 #pragma unroll
-          for (int bm = 0; bm < 4; ++bm)
+        for (int bm = 0; bm < kVB; ++bm)
 #pragma unroll
-            for (int q = 0; q < 16; ++q)
-              if (code == bm * 16 + q) zc = acc[bm][bn][q];
-          run_z[bn] = zc;
-        }
+          for (int q = 0; q < 4; ++q)
+            if (code == bm * 4 + q) zc = acc[bm][bn][q];
+        run_z[bn] = zc;
       }
     }
 #pragma unroll
-    for (int bm = 0; bm < 4; ++bm)
+    for (int bm = 0; bm < kVB; ++bm)
 #pragma unroll
-      for (int bn = 0; bn < kNB; ++bn)
+      for (int bn = 0; bn < kTB; ++bn)
 #pragma unroll
-        for (int q = 0; q < 16; ++q) acc[bm][bn][q] = 0.f;
+        for (int q = 0; q < 4; ++q) acc[bm][bn][q] = 0.f;
   };
 
-  // Gradient mode: G = g (1[v == y] - p) for the 4 x kNB blocks of this wave,
-  // rounded to bf16.  A lane holds runs of 4 consecutive vocabulary entries
-  // of its token row, 8 entries apart; lanes l and l + 32 hold the two
-  // halves of each 8-entry chunk.  G is stored chunk-major, so one 8-byte
-  // store per run covers 512 contiguous bytes across the wave (32 token
-  // rows x one chunk).  Rows >= V hold -inf, so p = 0 and G = 0 there, which
+  // Gradient mode: G = g (1[v == y] - p) for the kVB x kTB blocks of this
+  // wave, rounded to bf16.  In each block a lane holds 4 consecutive
+  // vocabulary entries of its token row: half of an 8-entry chunk (lane
+  // groups 0 and 1 hold the two halves of one chunk, groups 2 and 3 those of
+  // the next).  G is stored chunk-major, so one 8-byte store per block covers
+  // two runs of 256 contiguous bytes across the wave (16 token rows x one
+  // chunk each).  Rows >= V hold -inf, so p = 0 and G = 0 there, which
   // zero-fills the columns up to g_cols.
   auto grad_epilogue = [&](int64_t vt) {
     const int vbase = static_cast<int>(vt * kTileV) + wm * 128;   // V < 2^31
 #pragma unroll
-    for (int bn = 0; bn < kNB; ++bn) {
-      const int64_t e = rt * kTileN + wn * kWaveN + bn * 32 + col;
+    for (int bn = 0; bn < kTB; ++bn) {
+      const int64_t e = rt * kTileN + wn * kWaveN + bn * 16 + r16;
       const bool live = e < n_s;   // rows n_s .. round_up(n_s, 64) - 1 are written as zeros
       uint16_t* gcol = p.g_out + e * 8;   // chunk c of this row: gcol + c * g_ld * 8
       const float gneg = -g_up[bn];
 #pragma unroll
-      for (int bm = 0; bm < 4; ++bm) {
-        // element q of this lane's block is column v0 + 8 (q / 4) + q % 4
-        const int v0 = vbase + bm * 32 + 4 * half;
-        float gv[16];
+      for (int bm = 0; bm < kVB; ++bm) {
+        const int v0 = vbase + bm * 16 + 4 * grp;   // element q is column v0 + q
+        float gv[4];
 #pragma unroll
-        for (int q = 0; q < 16; ++q)
+        for (int q = 0; q < 4; ++q)
           gv[q] = gneg * fast_exp2(__builtin_fmaf(acc[bm][bn][q], kLog2e, -g_lse[bn]));
         // The sampled token's column gets g (1 - p) instead: at most one
         // element per row, so the branch is rarely taken by any lane.
         const int dt = tok[bn] - v0;
-        if (static_cast<unsigned>(dt) < 28u && (dt & 4) == 0) {
-          const int qi = (dt >> 3) * 4 + (dt & 3);
+        if (static_cast<unsigned>(dt) < 4u) {
 #pragma unroll
-          for (int q = 0; q < 16; ++q)
-            if (q == qi) gv[q] = g_up[bn] * (1.f - fast_exp2(__builtin_fmaf(acc[bm][bn][q], kLog2e, -g_lse[bn])));
+          for (int q = 0; q < 4; ++q)
+            if (q == dt) gv[q] = g_up[bn] * (1.f - fast_exp2(__builtin_fmaf(acc[bm][bn][q], kLog2e, -g_lse[bn])));
         }
-        uint32_t pk[4][2];   // [run jr][pair]: rows 8 jr + 4 half + {0,1 | 2,3}
+        uint32_t pk[2];
 #pragma unroll
-        for (int jr = 0; jr < 4; ++jr)
-#pragma unroll
-          for (int r = 0; r < 4; r += 2) {
-            const uint32_t w = static_cast<uint32_t>(__builtin_bit_cast(uint16_t, static_cast<__bf16>(gv[jr * 4 + r]))) |
-                               (static_cast<uint32_t>(__builtin_bit_cast(uint16_t, static_cast<__bf16>(gv[jr * 4 + r + 1])))
-                                << 16);
-            pk[jr][r / 2] = live ? w : 0u;
-          }
-        // run jr of this lane = entries v0 + 8 jr .. +3 = bytes 8 half .. +7 of chunk (v0 / 8 + jr)
-        if (e < n_s_pad && vbase + bm * 32 < p.g_cols) {
-          uint16_t* dst = gcol + ((vbase + bm * 32) / 8) * p.g_ld * 8 + 4 * half;
-#pragma unroll
-          for (int jr = 0; jr < 4; ++jr)
-            *reinterpret_cast<uint2*>(dst + jr * p.g_ld * 8) = make_uint2(pk[jr][0], pk[jr][1]);
+        for (int r = 0; r < 4; r += 2) {
+          const uint32_t w = static_cast<uint32_t>(__builtin_bit_cast(uint16_t, static_cast<__bf16>(gv[r]))) |
+                             (static_cast<uint32_t>(__builtin_bit_cast(uint16_t, static_cast<__bf16>(gv[r + 1])))
+                              << 16);
+          pk[r / 2] = live ? w : 0u;
         }
+        // entries v0 .. v0 + 3 = bytes 8 (grp & 1) .. + 7 of chunk v0 / 8
+        if (e < n_s_pad && vbase + bm * 16 < p.g_cols)
+          *reinterpret_cast<uint2*>(gcol + (v0 / 8) * p.g_ld * 8 + 4 * (grp & 1)) = make_uint2(pk[0], pk[1]);
       }
     }
 #pragma unroll
-    for (int bm = 0; bm < 4; ++bm)
+    for (int bm = 0; bm < kVB; ++bm)
 #pragma unroll
-      for (int bn = 0; bn < kNB; ++bn)
+      for (int bn = 0; bn < kTB; ++bn)
 #pragma unroll
-        for (int q = 0; q < 16; ++q) acc[bm][bn][q] = 0.f;
+        for (int q = 0; q < 4; ++q) acc[bm][bn][q] = 0.f;
   };
 
-
   // ---- pipelined main loop over (V-tile, K-slice) ------------------------
+  // A K-slice is 2 K-steps x 4 quarters; quarter pr multiplies the W
+  // fragments of vocabulary blocks 2 pr, 2 pr + 1 with the kTB hidden-state
+  // fragments.  Each quarter first reads what the next one needs: the next
+  // quarter's two W fragments (alternating buffers fa[0], fa[1]) and, during
+  // K-step 0, one hidden-state fragment of K-step 1 (fb[1]).  The slice's
+  // last quarter waits for the next slice's DMA and the workgroup barrier,
+  // reads the next slice's first W fragments and all of its K-step-0 hidden
+  // fragments (fb[0]), and issues the DMA of the slice after next into the
+  // stage just released, spread between its MFMAs.
   const int n_pre = n_iter < kStages ? n_iter : kStages;
   for (int sl = 0; sl < n_pre; ++sl) issue(sl);
   wait_dma(n_pre - 1);
   raw_barrier();
   if (k_tail && nk == 1) { clear_k_tail(0); raw_barrier(); }
 
-  // The 4 x kNB MFMAs of one sub-step.
-  auto mfma_step = [&](const uint4 (&a)[4], const uint4 (&b)[kNB]) {
-#pragma unroll
-    for (int j = 0; j < 4 * kNB; ++j) M::run(a[j / kNB], b[j % kNB], acc[j / kNB][j % kNB]);
-  };
-
-  uint4 fa[2][4], fb[2][kNB];
+  uint4 fa[2][2], fb[2][kTB];
   int it = 0;   // global slice counter
   for (int64_t vt = vt0; vt < vt1; ++vt) {
-    load_frags(it, 0, fa[0], fb[0]);
+    load_a(it, 0, 0, fa[0]);
+#pragma unroll
+    for (int bn = 0; bn < kTB; ++bn) load_b(it, 0, bn, fb[0][bn]);
     for (int kt = 0; kt < nk; ++kt, ++it) {
+      // K-step 0
 #pragma unroll
-      for (int kk = 0; kk < kSub; ++kk) {
-        const int cur = kk & 1;
-        if (kk + 1 < kSub) {
-          load_frags(it, kk + 1, fa[cur ^ 1], fb[cur ^ 1]);
-          // keep the fragment reads for the next sub-step ahead of this
-          // sub-step's MFMAs, so their LDS latency hides under matrix work
-          __builtin_amdgcn_sched_barrier(0);
-          mfma_step(fa[cur], fb[cur]);
-        } else if (KTAIL) {
-          // every read of slice `it` is issued: wait for slice it+1, then
-          // recycle this slice's stage for slice it+kStages.  On the call's
-          // last slice this waits for nothing and the fragment reads below
-          // fetch stale (in-bounds, unused) LDS: keeping this path
-          // unconditional leaves no control-flow join before the MFMAs.
-          const int after = n_iter - 2 - it;
-          wait_dma(after < kStages - 2 ? after : kStages - 2);
-          raw_barrier();
-          if (((it + 1) % nk) == nk - 1) { clear_k_tail(it + 1); raw_barrier(); }
-          if (it + kStages < n_iter) issue(it + kStages);
-          load_frags(it + 1, 0, fa[cur ^ 1], fb[cur ^ 1]);
-          __builtin_amdgcn_sched_barrier(0);
-          mfma_step(fa[cur], fb[cur]);
-        } else {
-          // As above, but the DMAs for slice it+kStages are spread between
-          // this sub-step's MFMAs so their issue overlaps matrix work.  They
-          // are unconditional: past the end of the work item they re-fetch
-          // the last slice into the stage just freed, which nothing reads.
-          wait_dma(kStages - 2);
-          raw_barrier();
-          const int nxt = it + kStages < n_iter ? it + kStages : n_iter - 1;
-          prep_issue(nxt);
-          load_frags(it + 1, 0, fa[cur ^ 1], fb[cur ^ 1]);
-          __builtin_amdgcn_sched_barrier(0);
-          constexpr int kM = 4 * kNB;                          // MFMAs per sub-step
-          constexpr int kEvery = kM / kDmaPerSlice > 0 ? kM / kDmaPerSlice : 1;
+      for (int pr = 0; pr < 4; ++pr) {
+        if (pr < 3) load_a(it, 0, pr + 1, fa[(pr + 1) & 1]);
+        else load_a(it, 1, 0, fa[0]);
+        load_b(it, 1, pr, fb[1][pr]);
+        // keep the fragment reads for the next quarter ahead of this
+        // quarter's MFMAs, so their LDS latency hides under matrix work
+        __builtin_amdgcn_sched_barrier(0);
+        quarter_mfma(fa[pr & 1], fb[0], pr);
+      }
+      // K-step 1, quarters 0-2
 #pragma unroll
-          for (int j = 0; j < kM; ++j) {
-            M::run(fa[cur][j / kNB], fb[cur][j % kNB], acc[j / kNB][j % kNB]);
-            if (j % kEvery == kEvery - 1 && j / kEvery < kDmaPerSlice) issue_one(j / kEvery, std::false_type{});
-          }
+      for (int pr = 0; pr < 3; ++pr) {
+        load_a(it, 1, pr + 1, fa[(pr + 1) & 1]);
+        __builtin_amdgcn_sched_barrier(0);
+        quarter_mfma(fa[pr & 1], fb[1], pr);
+      }
+      // K-step 1, quarter 3: the slice boundary.  Every read of slice `it`
+      // is issued: wait for slice it+1, then recycle this slice's stage.  On
+      // the work item's last slice this waits for nothing and the reads of
+      // "slice it+1" fetch stale (in-bounds, unused) LDS: keeping this path
+      // unconditional leaves no control-flow join before the MFMAs.
+      if (KTAIL) {
+        const int after = n_iter - 2 - it;
+        wait_dma(after < kStages - 2 ? after : kStages - 2);
+        raw_barrier();
+        if (((it + 1) % nk) == nk - 1) { clear_k_tail(it + 1); raw_barrier(); }
+        if (it + kStages < n_iter) issue(it + kStages);
+        load_a(it + 1, 0, 0, fa[0]);
 #pragma unroll
-          for (int j = kM / kEvery; j < kDmaPerSlice; ++j) issue_one(j, std::false_type{});
+        for (int bn = 0; bn < kTB; ++bn) load_b(it + 1, 0, bn, fb[0][bn]);
+        __builtin_amdgcn_sched_barrier(0);
+        quarter_mfma(fa[1], fb[1], 3);
+      } else {
+        // As above, but the DMAs for slice it+kStages are spread between
+        // this quarter's MFMAs so their issue overlaps matrix work.  They are
+        // unconditional: past the end of the work item they re-fetch the last
+        // slice into the stage just freed, which nothing reads.
+        wait_dma(kStages - 2);
+        raw_barrier();
+        const int nxt = it + kStages < n_iter ? it + kStages : n_iter - 1;
+        prep_issue(nxt);
+        load_a(it + 1, 0, 0, fa[0]);
+#pragma unroll
+        for (int bn = 0; bn < kTB; ++bn) load_b(it + 1, 0, bn, fb[0][bn]);
+        __builtin_amdgcn_sched_barrier(0);
+        constexpr int kM = 2 * kTB;                          // MFMAs per quarter
+        constexpr int kEvery = kM / kDmaPerSlice > 0 ? kM / kDmaPerSlice : 1;
+#pragma unroll
+        for (int j = 0; j < kM; ++j) {
+          M::run(fa[1][j / kTB], fb[1][j % kTB], acc[6 + j / kTB][j % kTB]);
+          if (j % kEvery == kEvery - 1 && j / kEvery < kDmaPerSlice) issue_one(j / kEvery, std::false_type{});
         }
+#pragma unroll
+        for (int j = kM / kEvery; j < kDmaPerSlice; ++j) issue_one(j, std::false_type{});
       }
     }
     if (GRAD) {
       if ((vt + 1) * kTileV > V) {
         // rows >= V: -inf, so that they contribute G = 0
 #pragma unroll
-        for (int bm = 0; bm < 4; ++bm)
+        for (int bm = 0; bm < kVB; ++bm)
 #pragma unroll
-          for (int bn = 0; bn < kNB; ++bn)
+          for (int bn = 0; bn < kTB; ++bn)
 #pragma unroll
-            for (int q = 0; q < 16; ++q)
-              if (vt * kTileV + wm * 128 + bm * 32 + acc_row(q, half) >= V) acc[bm][bn][q] = kNegInf;
+            for (int q = 0; q < 4; ++q)
+              if (vt * kTileV + wm * 128 + bm * 16 + 4 * grp + q >= V) acc[bm][bn][q] = kNegInf;
       }
       grad_epilogue(vt);
     } else if ((vt + 1) * kTileV <= V) {
@@ -474,23 +535,26 @@ __global__ __launch_bounds__(kThreads, 1) void lmhead_logprob_kernel(LmheadArgs 
   __syncthreads();
   if (GRAD) return;
 
-  // ---- merge the two lane halves, then the two vocabulary waves -----------
+  // ---- merge the four lane groups, then the two vocabulary waves ----------
 #pragma unroll
-  for (int bn = 0; bn < kNB; ++bn) {
-    const float m2 = __shfl_xor(run_m[bn], 32);
-    const float s2 = __shfl_xor(run_s[bn], 32);
-    const float z2 = __shfl_xor(run_z[bn], 32);
-    const float t2 = ENT ? __shfl_xor(run_t[bn], 32) : 0.f;
-    combine(run_m[bn], run_s[bn], run_z[bn], run_t[bn], m2, s2, z2, t2);
+  for (int bn = 0; bn < kTB; ++bn) {
+#pragma unroll
+    for (int x = 16; x <= 32; x <<= 1) {
+      const float m2 = __shfl_xor(run_m[bn], x);
+      const float s2 = __shfl_xor(run_s[bn], x);
+      const float z2 = __shfl_xor(run_z[bn], x);
+      const float t2 = ENT ? __shfl_xor(run_t[bn], x) : 0.f;
+      combine(run_m[bn], run_s[bn], run_z[bn], run_t[bn], m2, s2, z2, t2);
+    }
   }
   float* xm = reinterpret_cast<float*>(&lds[0][0][0]);
   float* xs = xm + kTileN;
   float* xz = xs + kTileN;
   float* xt = xz + kTileN;
-  if (wm == 1 && half == 0) {
+  if (wm == 1 && grp == 0) {
 #pragma unroll
-    for (int bn = 0; bn < kNB; ++bn) {
-      const int tcol = wn * kWaveN + bn * 32 + col;
+    for (int bn = 0; bn < kTB; ++bn) {
+      const int tcol = wn * kWaveN + bn * 16 + r16;
       xm[tcol] = run_m[bn];
       xs[tcol] = run_s[bn];
       xz[tcol] = run_z[bn];
@@ -498,10 +562,10 @@ __global__ __launch_bounds__(kThreads, 1) void lmhead_logprob_kernel(LmheadArgs 
     }
   }
   __syncthreads();
-  if (wm == 0 && half == 0) {
+  if (wm == 0 && grp == 0) {
 #pragma unroll
-    for (int bn = 0; bn < kNB; ++bn) {
-      const int tcol = wn * kWaveN + bn * 32 + col;
+    for (int bn = 0; bn < kTB; ++bn) {
+      const int tcol = wn * kWaveN + bn * 16 + r16;
       float m = run_m[bn], s = run_s[bn], z = run_z[bn], t = run_t[bn];
       combine(m, s, z, t, xm[tcol], xs[tcol], xz[tcol], ENT ? xt[tcol] : 0.f);
       const int64_t e = rt * kTileN + tcol;

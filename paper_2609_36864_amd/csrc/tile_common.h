@@ -12,6 +12,7 @@ namespace tile {
 
 typedef __bf16 bf16x8_t __attribute__((ext_vector_type(8)));
 typedef float f32x16_t __attribute__((ext_vector_type(16)));
+typedef float f32x4_t __attribute__((ext_vector_type(4)));
 
 constexpr int kWaves = 8;                           // two waves per SIMD
 constexpr int kThreads = 64 * kWaves;
