@@ -80,7 +80,7 @@ __device__ __forceinline__ void combine(float& m, float& s, float& z, float& t, 
 // The MFMA shape of this kernel: v_mfma_f32_16x16x32_bf16 (fp32 inputs: four
 // v_mfma_f32_16x16x4_f32 over one 16-byte fragment).  A fragment is 16 rows
 // of one operand: lane l holds row (l mod 16) and the 16-byte chunk
-// (4 ks + l div 16) of the K-slice, i.e. 8 bf16 (4 fp32) consecutive K
+// (4 ks + sigma(l div 16)) of the K-slice (see the fragment reads), i.e. 8 bf16 (4 fp32) consecutive K
 // values; A and B fragments take the same K positions, so the contraction is
 // exact whatever order the hardware sums them in.  The 16 x 16 fp32 result
 // block sits in 4 registers per lane: column (l mod 16), rows
@@ -291,8 +291,15 @@ __global__ __launch_bounds__(kThreads, 1) void lmhead_logprob_kernel(LmheadArgs 
   // ---- fragment reads ------------------------------------------------------
   // Fragments start at multiples of 16 rows, so a fragment row's swizzle is
   // that of (lane mod 16): one per-lane offset per K-step, plus immediates.
-  const int frag_lane[kKSteps] = {(r16 * kChunks + ((0 + grp) ^ row_xor(r16))),
-                                  (r16 * kChunks + ((4 + grp) ^ row_xor(r16)))};
+  // Lane group g reads chunk 4 ks + sigma(g), sigma = (0, 2, 1, 3): a
+  // ds_read_b128 serves lanes i..i+7 together with lanes i+32..i+39, i.e.
+  // groups g and g + 2 of the same 8 rows, and those must read chunks c and
+  // c ^ 1, which the row swizzle places in disjoint bank sets (chunks c and
+  // c + 2 would collide two-way).  A and B use the same mapping, so the
+  // K positions still pair up.
+  const int kchunk = ((grp & 1) << 1) | (grp >> 1);
+  const int frag_lane[kKSteps] = {(r16 * kChunks + ((0 + kchunk) ^ row_xor(r16))),
+                                  (r16 * kChunks + ((4 + kchunk) ^ row_xor(r16)))};
   // the two W fragments (vocabulary blocks 2 pr, 2 pr + 1) of quarter pr of K-step ks
   auto load_a = [&](int slice, int ks, int pr, uint4 (&dst)[2]) {
     const uint4* base = &lds[slice % kStages][0][frag_lane[ks]];
