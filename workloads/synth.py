@@ -24,8 +24,10 @@ datasets are not available, so hidden states are drawn synthetically:
 
 Random streams are keyed by (seed, stream, chunk), so every chunk is
 reproducible on its own and the result does not depend on thread counts.
-Generation runs on the CPU with torch's generator (deterministic across
-thread counts); bf16 values are produced by round-to-nearest-even.
+Generation runs on the CPU with torch's generator; only operations whose
+results are the same on every x86 host are used (square roots are taken with
+NumPy: torch's CPU sqrt differs in the last bit between vendors); bf16 values
+are produced by round-to-nearest-even.
 """
 from __future__ import annotations
 
@@ -36,7 +38,7 @@ from typing import Dict, List, Optional
 import numpy as np
 import torch
 
-GENERATOR_VERSION = 1
+GENERATOR_VERSION = 2
 
 # Stream identifiers (fixed order; never renumber).
 _S_W, _S_H0, _S_NOISE, _S_TOK, _S_PLANT, _S_ALPHA, _S_MASK, _S_DUP = range(8)
@@ -197,11 +199,18 @@ def _hidden0_rows(cfg: Config, r: int, t0: int, t1: int, chunk: int) -> torch.Te
         z = torch.empty(n, cfg.d, dtype=torch.float32).normal_(generator=g)
         c = torch.empty(3, n, cfg.d, dtype=torch.float32).normal_(generator=g)
         chi2 = (c * c).sum(0)
-        x = z / torch.sqrt(chi2 / 3.0)
+        x = z / _sqrt(chi2 / 3.0)
     else:
         raise ValueError(cfg.hidden_dist)
-    rms = torch.sqrt((x * x).mean(dim=1, keepdim=True))
+    rms = _sqrt((x * x).mean(dim=1, keepdim=True))
     return x / rms
+
+
+def _sqrt(t: torch.Tensor) -> torch.Tensor:
+    """Correctly rounded square root (NumPy's, the hardware instruction).
+    torch's CPU sqrt gives different last bits on different x86 vendors, which
+    would make the generated inputs depend on the host."""
+    return torch.from_numpy(np.sqrt(t.contiguous().numpy()))
 
 
 def make_workload(name: str, **overrides) -> Workload:
@@ -300,3 +309,19 @@ def make_logp_pair(R: int, T: int, seed: int, mask_kind: str = "spans",
         for _ in range(nan_rows):
             lh[r, int(g.integers(0, T))] = np.float32("nan")
     return lo, lh, mask
+
+
+def input_digest(w: Workload) -> str:
+    """SHA-256 over a workload's inputs (W, both contexts' hidden rows,
+    tokens, mask), so that stored expected values can be tied to the exact
+    inputs they were computed from."""
+    import hashlib
+    h = hashlib.sha256()
+    h.update(f"{w.cfg.name} v{GENERATOR_VERSION} {tuple(w.hidden.shape)} {w.cfg.V} {w.cfg.dtype}".encode())
+    for t in (w.W, w.hidden, w.tokens, w.mask):
+        flat = t.contiguous().view(-1)
+        step = 1 << 26   # elements per update (bounded temporary memory)
+        for i in range(0, flat.numel(), step):
+            h.update(flat[i:i + step].view(torch.uint8).numpy().tobytes() if t.dtype == torch.bfloat16
+                     else flat[i:i + step].numpy().tobytes())
+    return h.hexdigest()
