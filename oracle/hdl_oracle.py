@@ -335,15 +335,36 @@ def group_advantages(rewards: np.ndarray) -> np.ndarray:
     return R - R.mean(axis=1, keepdims=True)
 
 
+def trained_tokens(traj, n_traj: int, loss_mask=None, pos=None, start=None) -> int:
+    """Number of tokens the policy loss trains on: in the loss mask, with a
+    trajectory index in [0, n_traj), and (given positions) at or after their
+    trajectory's first trained position -- a continuation trains only its
+    newly sampled suffix (Sec. 3.3)."""
+    traj = np.asarray(traj).astype(np.int64)
+    count = 0
+    for i in range(traj.shape[0]):
+        j = traj[i]
+        if not (0 <= j < n_traj) or (loss_mask is not None and loss_mask[i] == 0):
+            continue
+        if pos is not None and pos[i] < start[j]:
+            continue
+        count += 1
+    return count
+
+
 def policy_loss_grad(adv, traj, logp_new, logp_old, loss_mask=None, pos=None, start=None,
-                     eps_low: float = 0.2, eps_high: float = 0.28, scale: float = 1.0):
+                     eps_low: float = 0.2, eps_high: float = 0.28, scale: Optional[float] = 1.0):
     """Per-token loss l = -scale * min(r A, clip(r, 1 - eps_low, 1 + eps_high) A)
     with r = exp(logp_new - logp_old), and g = dl/dlogp_new (Sec. 4.1
     "Training"); tokens outside the loss mask, before their trajectory's
     first trained position (a continuation's reused prefix, Sec. 3.3) or
-    with an out-of-range trajectory index give 0.  Returns (g, l)."""
+    with an out-of-range trajectory index give 0.  scale=None is the
+    token-level aggregation of Sec. 4.1: the mean over the trained tokens,
+    scale = 1 / max(1, trained_tokens(...)).  Returns (g, l)."""
     adv = np.asarray(adv, dtype=np.float64)
     traj = np.asarray(traj).astype(np.int64)
+    if scale is None:
+        scale = 1.0 / max(1, trained_tokens(traj, adv.shape[0], loss_mask, pos, start))
     n = traj.shape[0]
     g = np.zeros(n)
     loss = np.zeros(n)

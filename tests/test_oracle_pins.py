@@ -631,3 +631,51 @@ def test_non_finite_hidden_row_gives_nan_for_that_row_only():
         lp, lse = O.token_logprobs(H, W, y)
     assert np.isnan(lp[1]) and np.isnan(lp[3]) and np.isnan(lse[1])
     assert np.array_equal(lp[[0, 2]], clean[[0, 2]])
+
+
+def test_token_level_aggregation_counts_trained_tokens():
+    # Hand-worked (Sec. 4.1 "Training": token-level aggregation; Sec. 3.3: a
+    # continuation trains only its suffix).  Two trajectories, the second a
+    # continuation branched at position 2; token 1 is outside the loss mask,
+    # tokens 2 and 3 are the continuation's reused prefix, token 5 names a
+    # trajectory that does not exist: tokens 0 and 4 are trained, so the
+    # token-level mean divides by 2.
+    adv = np.array([0.5, -1.0])
+    traj = np.array([0, 0, 1, 1, 1, 5])
+    pos = np.array([0, 1, 0, 1, 2, 0])
+    start = np.array([0, 2])
+    mask = np.array([1, 0, 1, 1, 1, 1], np.uint8)
+    lo_ = np.full(6, -1.0)
+    assert O.trained_tokens(traj, 2, mask, pos, start) == 2
+    g, l = O.policy_loss_grad(adv, traj, lo_, lo_, mask, pos, start, scale=None)
+    # on policy (r = 1): g = -A / 2 on the trained tokens, 0 elsewhere
+    assert g.tolist() == [-0.25, 0.0, 0.0, 0.0, 0.5, 0.0]
+    assert l.tolist() == [-0.25, 0.0, 0.0, 0.0, 0.5, 0.0]
+    # nothing trained: the divisor is 1, every factor 0
+    assert O.trained_tokens(traj, 2, np.zeros(6, np.uint8), pos, start) == 0
+    g0, _ = O.policy_loss_grad(adv, traj, lo_, lo_, np.zeros(6, np.uint8), pos, start, scale=None)
+    assert np.all(g0 == 0.0)
+
+
+def test_trained_token_count_per_trajectory():
+    # Counted trajectory by trajectory (positions at or past the trajectory's
+    # start among its masked-in tokens) instead of token by token; and the
+    # scale=None factors are the scale=1 factors divided by that count.
+    rng = np.random.default_rng(21)
+    n, n_traj = 3000, 40
+    traj = rng.integers(-3, n_traj + 3, n)
+    pos = rng.integers(0, 200, n)
+    start = rng.integers(0, 150, n_traj)
+    mask = (rng.random(n) < 0.85).astype(np.uint8)
+    want = 0
+    for j in range(n_traj):
+        mine = (traj == j) & (mask != 0)
+        want += int(np.count_nonzero(pos[mine] >= start[j]))
+    assert O.trained_tokens(traj, n_traj, mask, pos, start) == want
+    assert O.trained_tokens(traj, n_traj, mask) == int(np.count_nonzero((traj >= 0) & (traj < n_traj) & (mask != 0)))
+    adv = rng.normal(size=n_traj)
+    lo_ = rng.normal(size=n) * 0.1 - 2
+    ln = lo_ + rng.normal(size=n) * 0.3
+    g1, l1 = O.policy_loss_grad(adv, traj, ln, lo_, mask, pos, start, scale=1.0)
+    gm, lm = O.policy_loss_grad(adv, traj, ln, lo_, mask, pos, start, scale=None)
+    assert np.allclose(gm, g1 / want, rtol=1e-15, atol=0) and np.allclose(lm, l1 / want, rtol=1e-15, atol=0)
