@@ -556,6 +556,7 @@ def bench_group(args, w, hdl, dev) -> int:
     tmask = torch.from_numpy((rng.random(n_tok) < 0.9).astype(np.uint8)).to(dev)
     start = torch.zeros(n_traj, dtype=torch.int32, device=dev)
     grad = torch.empty(n_tok, dtype=torch.float32, device=dev)
+    n_trained = torch.empty(1, dtype=torch.int64, device=dev)
     torch.cuda.synchronize()
 
     def step():
@@ -566,8 +567,9 @@ def bench_group(args, w, hdl, dev) -> int:
         st = start.view(n_groups, G)
         st[:, roots_per_group:] = bpos.view(n_groups, -1)
         adv = hdl.group_advantages(rewards).view(-1)
+        # token-level mean over the trained tokens, counted on the device
         g, _ = hdl.policy_loss_grad(adv, traj, logp_new, logp_old, loss_mask=tmask, pos=pos, start=start,
-                                    scale=1.0 / n_tok)
+                                    n_trained=n_trained)
         return idx, count, g
 
     for _ in range(args.warmup):

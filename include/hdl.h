@@ -19,8 +19,8 @@
  *    every pointer must belong to that device.
  *  - Argument errors are reported synchronously by a negative return value,
  *    before anything is enqueued.  A failed kernel launch returns
- *    HDL_ERR_HIP.  hdl_last_error() describes the most recent failure of the
- *    calling thread.  No C++ exception crosses this boundary.
+ *    HDL_ERR_HIP.  hdl_last_hip_error() describes the most recent failure of
+ *    the calling thread (an argument error or a HIP error).  No C++ exception crosses this boundary.
  *  - Row-major layouts throughout; "[a, b]" means a rows of b contiguous
  *    elements.
  */
@@ -36,7 +36,9 @@ extern "C" {
 
 /* Element type of `hidden` and `w_vocab`.  Accumulation, the log-sum-exp and
  * all outputs are fp32 for both. */
-typedef enum { HDL_F32 = 0, HDL_BF16 = 1 } hdl_dtype;
+/* Element type of hidden states and the vocabulary projection (the last
+ * enumerator only keeps the type int-sized; it is not a valid dtype). */
+typedef enum { HDL_F32 = 0, HDL_BF16 = 1, HDL_DTYPE_INT_ = 0x7fffffff } hdl_dtype;
 
 enum {
   HDL_OK = 0,
@@ -55,7 +57,7 @@ enum {
  * scored rows and the per-vocabulary-chunk partial log-sum-exp states.
  */
 size_t hdl_token_logprobs_workspace_size(int64_t n_rows, int64_t d, int64_t vocab,
-                                         int dtype);
+                                         hdl_dtype dtype);
 
 /*
  * Teacher-forced log-likelihood of each row's sampled token (Eq. 1):
@@ -97,7 +99,7 @@ size_t hdl_token_logprobs_workspace_size(int64_t n_rows, int64_t d, int64_t voca
  */
 int hdl_token_logprobs(const void* hidden, const void* w_vocab, const int32_t* tokens,
                        const uint8_t* mask, int64_t n_rows, int64_t d, int64_t vocab,
-                       int dtype, float* logp, float* lse_out, void* workspace,
+                       hdl_dtype dtype, float* logp, float* lse_out, void* workspace,
                        size_t workspace_bytes, void* stream);
 
 /*
@@ -118,7 +120,7 @@ int hdl_token_logprobs(const void* hidden, const void* w_vocab, const int32_t* t
  */
 int hdl_token_logprobs_entropy(const void* hidden, const void* w_vocab, const int32_t* tokens,
                                const uint8_t* mask, int64_t n_rows, int64_t d, int64_t vocab,
-                               int dtype, float* logp, float* lse_out, float* entropy,
+                               hdl_dtype dtype, float* logp, float* lse_out, float* entropy,
                                void* workspace, size_t workspace_bytes, void* stream);
 
 /*
@@ -145,7 +147,7 @@ int hdl_token_logprobs_entropy(const void* hidden, const void* w_vocab, const in
  */
 int hdl_token_logprobs_noalloc(const void* hidden, const void* w_vocab, const int32_t* tokens,
                                const uint8_t* mask, int64_t n_rows, int64_t d, int64_t vocab,
-                               int dtype, float* logp, float* lse_out, void* stream);
+                               hdl_dtype dtype, float* logp, float* lse_out, void* stream);
 
 /*
  * Hindsight-divergence score and per-root branch-point selection (Eq. 2 and
@@ -194,7 +196,7 @@ int hdl_select_top_k(const float* values, const uint8_t* mask, int64_t n_roots, 
  * 0.4 GB for 32768 rows at d = 2048).
  */
 size_t hdl_token_logprobs_backward_workspace_size(int64_t n_rows, int64_t d, int64_t vocab,
-                                                  int dtype);
+                                                  hdl_dtype dtype);
 
 /*
  * Backward pass of hdl_token_logprobs for a loss L = sum_n g_n log p_n(y_n)
@@ -227,7 +229,7 @@ size_t hdl_token_logprobs_backward_workspace_size(int64_t n_rows, int64_t d, int
  */
 int hdl_token_logprobs_backward(const void* hidden, const void* w_vocab, const int32_t* tokens,
                                 const uint8_t* mask, const float* lse, const float* grad_logp,
-                                int64_t n_rows, int64_t d, int64_t vocab, int dtype,
+                                int64_t n_rows, int64_t d, int64_t vocab, hdl_dtype dtype,
                                 float* grad_hidden, float* grad_w, int accumulate_w,
                                 void* workspace, size_t workspace_bytes, void* stream);
 
@@ -301,20 +303,27 @@ int hdl_group_advantages(const float* rewards, int64_t n_groups, int32_t group_s
  *  0 for a root, the branch position for a continuation (only the newly
  *  sampled suffix is trained, Sec. 3.3).
  *  loss_mask [n_tokens] uint8 or NULL (policy-generated tokens).
- *  scale  the aggregation factor, e.g. 1 / (number of trained tokens).
+ *  scale  the aggregation factor; scale <= 0 asks for the token-level mean of
+ *         Sec. 4.1 ("Training"), scale = 1 / max(1, T) with T the number of
+ *         trained tokens (in the mask, of a trajectory in [0, n_traj), at or
+ *         after its first trained position), counted on the device.
  *  grad_logp [n_tokens] fp32 out (0 for untrained tokens); loss [n_tokens]
  *  fp32 out (scale * l, 0 for untrained tokens) or NULL.
+ *  n_trained  device int64 [1] out or NULL: T; required (and used as the
+ *         count's scratch) when scale <= 0.  8-byte aligned.
+ *  A NaN scale, or scale <= 0 without n_trained, is HDL_ERR_INVALID_ARG.
  */
 int hdl_policy_loss_grad(const float* adv, int64_t n_traj, const int32_t* traj, const int32_t* pos,
                          const int32_t* start, const float* logp_new, const float* logp_old,
                          const uint8_t* loss_mask, int64_t n_tokens, float eps_low, float eps_high,
-                         float scale, float* grad_logp, float* loss, void* stream);
+                         float scale, float* grad_logp, float* loss, int64_t* n_trained, void* stream);
 
 /* Static description of a status code. */
 const char* hdl_status_string(int status);
 
-/* Description of the calling thread's most recent failure ("" if none). */
-const char* hdl_last_error(void);
+/* Description of the calling thread's most recent failure, an argument
+ * error or a HIP error ("" if the last call succeeded); thread-local. */
+const char* hdl_last_hip_error(void);
 
 /* ABI version of this library (increments on incompatible changes). */
 int hdl_abi_version(void);

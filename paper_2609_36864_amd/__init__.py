@@ -79,15 +79,15 @@ def load_library() -> ctypes.CDLL:
     L.hdl_group_advantages.argtypes = [c_vp, c_i64, ctypes.c_int32, c_vp, c_vp]
     L.hdl_group_advantages.restype = ctypes.c_int
     L.hdl_policy_loss_grad.argtypes = [c_vp, c_i64, c_vp, c_vp, c_vp, c_vp, c_vp, c_vp, c_i64, ctypes.c_float,
-                                       ctypes.c_float, ctypes.c_float, c_vp, c_vp, c_vp]
+                                       ctypes.c_float, ctypes.c_float, c_vp, c_vp, c_vp, c_vp]
     L.hdl_policy_loss_grad.restype = ctypes.c_int
     L.hdl_select_branch_points.argtypes = [c_vp, c_vp, c_vp, c_i64, c_i64, ctypes.c_int32,
                                            c_vp, c_vp, c_vp, c_vp, c_vp]
     L.hdl_select_branch_points.restype = ctypes.c_int
     L.hdl_status_string.argtypes = [ctypes.c_int]
     L.hdl_status_string.restype = ctypes.c_char_p
-    L.hdl_last_error.argtypes = []
-    L.hdl_last_error.restype = ctypes.c_char_p
+    L.hdl_last_hip_error.argtypes = []
+    L.hdl_last_hip_error.restype = ctypes.c_char_p
     L.hdl_abi_version.argtypes = []
     L.hdl_abi_version.restype = ctypes.c_int
     L.hdl_profile_enable.argtypes = [ctypes.c_int]
@@ -103,7 +103,7 @@ def load_library() -> ctypes.CDLL:
 def _check(status: int) -> None:
     if status != 0:
         L = load_library()
-        msg = L.hdl_last_error().decode() or L.hdl_status_string(status).decode()
+        msg = L.hdl_last_hip_error().decode() or L.hdl_status_string(status).decode()
         raise HdlError(status, msg)
 
 
@@ -404,9 +404,11 @@ def group_advantages(rewards: torch.Tensor) -> torch.Tensor:
 def policy_loss_grad(adv: torch.Tensor, traj: torch.Tensor, logp_new: torch.Tensor, logp_old: torch.Tensor, *,
                      loss_mask: Optional[torch.Tensor] = None, pos: Optional[torch.Tensor] = None,
                      start: Optional[torch.Tensor] = None, eps_low: float = 0.2, eps_high: float = 0.28,
-                     scale: Optional[float] = None):
+                     scale: Optional[float] = None, n_trained: Optional[torch.Tensor] = None):
     """Per-token g = dL/dlog pi of the clipped token-level policy loss and the
-    per-token loss; scale defaults to 1 / (number of tokens in the mask)."""
+    per-token loss.  scale=None: the token-level mean over the trained tokens,
+    counted on the device into n_trained (int64 [1], allocated if not given).
+    Returns (grad, loss)."""
     L = load_library()
     _dev_2d("adv", adv, torch.float32)
     n = traj.numel()
@@ -422,14 +424,18 @@ def policy_loss_grad(adv: torch.Tensor, traj: torch.Tensor, logp_new: torch.Tens
     if pos is not None:
         _dev_2d("pos", pos, torch.int32, (n,))
         _dev_2d("start", start, torch.int32, (adv.numel(),))
-    if scale is None:
-        scale = 1.0 / max(1, int(n if loss_mask is None else loss_mask.sum().item()))
+    if scale is not None and not scale > 0:
+        raise ValueError("scale must be positive (None: token-level mean)")
+    if scale is None and n_trained is None:
+        n_trained = torch.empty(1, dtype=torch.int64, device=traj.device)
+    if n_trained is not None:
+        _dev_2d("n_trained", n_trained, torch.int64, (1,))
     grad = torch.empty(n, dtype=torch.float32, device=traj.device)
     loss = torch.empty_like(grad)
     _check(L.hdl_policy_loss_grad(adv.data_ptr(), adv.numel(), traj.data_ptr(), _ptr(pos), _ptr(start),
                                   logp_new.data_ptr(), logp_old.data_ptr(), _ptr(loss_mask), n, float(eps_low),
-                                  float(eps_high), float(scale), grad.data_ptr(), loss.data_ptr(),
-                                  _stream_handle(traj.device)))
+                                  float(eps_high), 0.0 if scale is None else float(scale), grad.data_ptr(),
+                                  loss.data_ptr(), _ptr(n_trained), _stream_handle(traj.device)))
     return grad, loss
 
 

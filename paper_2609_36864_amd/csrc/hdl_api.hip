@@ -96,7 +96,7 @@ struct TimedLaunch {
 
 extern "C" {
 
-size_t hdl_token_logprobs_workspace_size(int64_t n_rows, int64_t d, int64_t vocab, int dtype) {
+size_t hdl_token_logprobs_workspace_size(int64_t n_rows, int64_t d, int64_t vocab, hdl_dtype dtype) {
   if (n_rows <= 0 || d <= 0 || vocab <= 0 || n_rows > INT32_MAX || vocab > INT32_MAX) return 0;
   if (dtype != HDL_F32 && dtype != HDL_BF16) return 0;
   const int esz = dtype == HDL_BF16 ? 2 : 4;
@@ -111,7 +111,7 @@ namespace {
 // Argument checks shared by the log-probability entry points; on success
 // *esz is the element size.  Nothing is launched.
 int check_stats_args(const char* fn, const void* hidden, const void* w_vocab, const int32_t* tokens,
-                     float* logp, int64_t n_rows, int64_t d, int64_t vocab, int dtype, int* esz) {
+                     float* logp, int64_t n_rows, int64_t d, int64_t vocab, hdl_dtype dtype, int* esz) {
   if (!hidden || !w_vocab || !tokens || !logp)
     return fail(HDL_ERR_INVALID_ARG, "%s: null hidden, w_vocab, tokens or logp", fn);
   if (n_rows <= 0 || d <= 0 || vocab <= 0)
@@ -200,7 +200,7 @@ int token_stats(const char* fn, const void* hidden, const void* w_vocab, const i
 
 // The workspace entry points: the caller's workspace, the default plan.
 int token_stats_ws(const char* fn, const void* hidden, const void* w_vocab, const int32_t* tokens,
-                   const uint8_t* mask, int64_t n_rows, int64_t d, int64_t vocab, int dtype, float* logp,
+                   const uint8_t* mask, int64_t n_rows, int64_t d, int64_t vocab, hdl_dtype dtype, float* logp,
                    float* lse_out, float* entropy, void* workspace, size_t workspace_bytes, void* stream) {
   g_last_error[0] = '\0';
   int esz = 0;
@@ -242,7 +242,7 @@ int scratch_on_current_device(const char* fn, char** out) {
 extern "C" {
 
 int hdl_token_logprobs(const void* hidden, const void* w_vocab, const int32_t* tokens,
-                       const uint8_t* mask, int64_t n_rows, int64_t d, int64_t vocab, int dtype,
+                       const uint8_t* mask, int64_t n_rows, int64_t d, int64_t vocab, hdl_dtype dtype,
                        float* logp, float* lse_out, void* workspace, size_t workspace_bytes,
                        void* stream) {
   return token_stats_ws("hdl_token_logprobs", hidden, w_vocab, tokens, mask, n_rows, d, vocab, dtype,
@@ -251,7 +251,7 @@ int hdl_token_logprobs(const void* hidden, const void* w_vocab, const int32_t* t
 
 int hdl_token_logprobs_entropy(const void* hidden, const void* w_vocab, const int32_t* tokens,
                                const uint8_t* mask, int64_t n_rows, int64_t d, int64_t vocab,
-                               int dtype, float* logp, float* lse_out, float* entropy,
+                               hdl_dtype dtype, float* logp, float* lse_out, float* entropy,
                                void* workspace, size_t workspace_bytes, void* stream) {
   if (!entropy) {
     g_last_error[0] = '\0';
@@ -262,7 +262,7 @@ int hdl_token_logprobs_entropy(const void* hidden, const void* w_vocab, const in
 }
 
 int hdl_token_logprobs_noalloc(const void* hidden, const void* w_vocab, const int32_t* tokens,
-                               const uint8_t* mask, int64_t n_rows, int64_t d, int64_t vocab, int dtype,
+                               const uint8_t* mask, int64_t n_rows, int64_t d, int64_t vocab, hdl_dtype dtype,
                                float* logp, float* lse_out, void* stream) {
   const char* fn = "hdl_token_logprobs_noalloc";
   g_last_error[0] = '\0';
@@ -330,9 +330,9 @@ const char* hdl_status_string(int status) {
   }
 }
 
-const char* hdl_last_error(void) { return g_last_error; }
+const char* hdl_last_hip_error(void) { return g_last_error; }
 
-int hdl_abi_version(void) { return 5; }
+int hdl_abi_version(void) { return 6; }
 
 int hdl_profile_enable(int on) {
   std::lock_guard<std::mutex> lk(g_prof.mu);
@@ -452,7 +452,7 @@ hdl::GemmArgs gemm_args(const void* a, int64_t lda, int a_layout, int64_t a_cols
 
 extern "C" {
 
-size_t hdl_token_logprobs_backward_workspace_size(int64_t n_rows, int64_t d, int64_t vocab, int dtype) {
+size_t hdl_token_logprobs_backward_workspace_size(int64_t n_rows, int64_t d, int64_t vocab, hdl_dtype dtype) {
   if (n_rows <= 0 || d <= 0 || vocab <= 0 || n_rows > INT32_MAX || vocab > INT32_MAX) return 0;
   if (dtype != HDL_BF16 || d % 8 != 0) return 0;
   if (vocab > kBwdMaxVocab || d > kBwdMaxD) return 0;
@@ -463,7 +463,7 @@ size_t hdl_token_logprobs_backward_workspace_size(int64_t n_rows, int64_t d, int
 
 int hdl_token_logprobs_backward(const void* hidden, const void* w_vocab, const int32_t* tokens,
                                 const uint8_t* mask, const float* lse, const float* grad_logp,
-                                int64_t n_rows, int64_t d, int64_t vocab, int dtype, float* grad_hidden,
+                                int64_t n_rows, int64_t d, int64_t vocab, hdl_dtype dtype, float* grad_hidden,
                                 float* grad_w, int accumulate_w, void* workspace, size_t workspace_bytes,
                                 void* stream) {
   const char* fn = "hdl_token_logprobs_backward";
@@ -646,7 +646,7 @@ int hdl_group_advantages(const float* rewards, int64_t n_groups, int32_t group_s
 int hdl_policy_loss_grad(const float* adv, int64_t n_traj, const int32_t* traj, const int32_t* pos,
                          const int32_t* start, const float* logp_new, const float* logp_old,
                          const uint8_t* loss_mask, int64_t n_tokens, float eps_low, float eps_high, float scale,
-                         float* grad_logp, float* loss, void* stream) {
+                         float* grad_logp, float* loss, int64_t* n_trained, void* stream) {
   const char* fn = "hdl_policy_loss_grad";
   g_last_error[0] = '\0';
   if (!adv || !traj || !logp_new || !logp_old || !grad_logp)
@@ -656,8 +656,13 @@ int hdl_policy_loss_grad(const float* adv, int64_t n_traj, const int32_t* traj, 
   if (n_traj <= 0 || n_tokens <= 0) return fail(HDL_ERR_INVALID_ARG, "%s: sizes must be positive", fn);
   if (n_tokens > (int64_t{1} << 38)) return fail(HDL_ERR_UNSUPPORTED, "%s: too many tokens", fn);
   if (!(eps_low >= 0.f) || !(eps_high >= 0.f)) return fail(HDL_ERR_INVALID_ARG, "%s: negative clip range", fn);
+  if (scale != scale) return fail(HDL_ERR_INVALID_ARG, "%s: scale is NaN", fn);
+  if (!(scale > 0.f) && !n_trained)
+    return fail(HDL_ERR_INVALID_ARG, "%s: scale <= 0 (token-level mean) needs n_trained", fn);
+  if (n_trained && !aligned(n_trained, 8)) return fail(HDL_ERR_INVALID_ARG, "%s: n_trained must be 8-byte aligned", fn);
   hipError_t e = hdl::launch_policy_grad(adv, traj, pos, start, logp_new, logp_old, loss_mask, n_tokens, n_traj,
-                                         eps_low, eps_high, scale, grad_logp, loss, static_cast<hipStream_t>(stream));
+                                         eps_low, eps_high, scale, grad_logp, loss, n_trained,
+                                         static_cast<hipStream_t>(stream));
   if (e != hipSuccess) return hip_fail(e, "policy-gradient kernel launch");
   return HDL_OK;
 }

@@ -112,6 +112,6 @@ hipError_t launch_advantages(const float* rewards, int64_t n_groups, int group_s
 hipError_t launch_policy_grad(const float* adv, const int32_t* traj, const int32_t* pos, const int32_t* start,
                               const float* logp_new, const float* logp_old, const uint8_t* loss_mask,
                               int64_t n_tokens, int64_t n_traj, float eps_low, float eps_high, float scale,
-                              float* grad, float* loss, hipStream_t stream);
+                              float* grad, float* loss, int64_t* n_trained, hipStream_t stream);
 
 }  // namespace hdl

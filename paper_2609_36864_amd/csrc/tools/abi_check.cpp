@@ -100,7 +100,7 @@ int main() {
       hipMalloc(&d_score, kRoots * kK * 4) != hipSuccess || hipMalloc(&d_delta, kRoots * kT * 4) != hipSuccess ||
       hipMalloc(&d_idx, kRoots * kK * 4) != hipSuccess || hipMalloc(&d_count, kRoots * 4) != hipSuccess ||
       hipMalloc(&d_ws, ws) != hipSuccess) {
-    std::printf("abi_check: FAILED: setup (%s)\n", hdl_last_error());
+    std::printf("abi_check: FAILED: setup (%s)\n", hdl_last_hip_error());
     return 1;
   }
 

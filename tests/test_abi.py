@@ -30,7 +30,7 @@ def test_header_declares_the_boundary():
     names = _declared_functions()
     for n in ("hdl_token_logprobs", "hdl_token_logprobs_entropy", "hdl_select_branch_points",
               "hdl_select_top_k", "hdl_token_logprobs_workspace_size", "hdl_status_string",
-              "hdl_last_error", "hdl_token_logprobs_backward", "hdl_token_logprobs_backward_workspace_size",
+              "hdl_last_hip_error", "hdl_token_logprobs_backward", "hdl_token_logprobs_backward_workspace_size",
               "hdl_select_constrained", "hdl_allocate_continuations", "hdl_group_advantages",
               "hdl_policy_loss_grad", "hdl_profile_enable", "hdl_profile_read", "hdl_profile_read_kind"):
         assert n in names
@@ -45,7 +45,7 @@ def test_status_strings(lib):
     assert lib.hdl_status_string(0) == b"ok"
     for s in (-1, -2, -3, -4):
         assert lib.hdl_status_string(s) not in (b"ok", b"unknown status")
-    assert lib.hdl_abi_version() == 5
+    assert lib.hdl_abi_version() == 6
 
 
 def test_workspace_size_rules(lib):
@@ -62,7 +62,7 @@ def test_logprobs_argument_errors(lib):
     call = lib.hdl_token_logprobs
     p = ctypes.c_void_p(4096)       # never dereferenced: validation fails first
     assert call(None, p, p, None, 4, 64, 10, 1, p, None, p, 1 << 20, None) == -1
-    assert b"null" in lib.hdl_last_error()
+    assert b"null" in lib.hdl_last_hip_error()
     assert call(p, p, p, None, 0, 64, 10, 1, p, None, p, 1 << 20, None) == -1
     assert call(p, p, p, None, 4, 64, 10, 5, p, None, p, 1 << 20, None) == -2
     assert call(p, p, p, None, 4, 12, 10, 1, p, None, p, 1 << 20, None) == -2
@@ -79,7 +79,7 @@ def test_select_argument_errors(lib):
     assert call(p, p, None, 0, 10, 2, p, p, p, None, None) == -1
     assert call(p, p, None, 1, 10, 0, p, p, p, None, None) == -1
     assert call(p, p, None, 1, 10, 1025, p, p, p, None, None) == -2
-    assert b"1025" in lib.hdl_last_error()
+    assert b"1025" in lib.hdl_last_hip_error()
 
 
 def test_entropy_and_value_topk_argument_errors(lib):
@@ -152,9 +152,14 @@ def test_group_construction_argument_errors(lib):
     pg.argtypes = [ctypes.c_void_p, ctypes.c_int64] + [ctypes.c_void_p] * 6 + [ctypes.c_int64, ctypes.c_float,
                                                                                 ctypes.c_float, ctypes.c_float,
                                                                                 ctypes.c_void_p, ctypes.c_void_p,
-                                                                                ctypes.c_void_p]
-    assert pg(p, 4, p, p, None, p, p, None, 10, 0.2, 0.28, 1.0, p, None, None) == -1   # pos without start
-    assert pg(p, 4, p, None, None, p, p, None, 10, -0.2, 0.28, 1.0, p, None, None) == -1
+                                                                                ctypes.c_void_p, ctypes.c_void_p]
+    assert pg(p, 4, p, p, None, p, p, None, 10, 0.2, 0.28, 1.0, p, None, None, None) == -1   # pos without start
+    assert pg(p, 4, p, None, None, p, p, None, 10, -0.2, 0.28, 1.0, p, None, None, None) == -1
+    # the token-level mean (scale <= 0) needs the device count; NaN scale
+    assert pg(p, 4, p, None, None, p, p, None, 10, 0.2, 0.28, 0.0, p, None, None, None) == -1
+    assert b"n_trained" in lib.hdl_last_hip_error()
+    assert pg(p, 4, p, None, None, p, p, None, 10, 0.2, 0.28, float("nan"), p, None, p, None) == -1
+    assert pg(p, 4, p, None, None, p, p, None, 10, 0.2, 0.28, 0.0, p, None, ctypes.c_void_p(0x1004), None) == -1
 
 
 def test_binding_rejects_host_tensors_before_any_launch():
@@ -180,4 +185,4 @@ def test_noalloc_argument_checks_before_any_hip_call(lib):
     assert f(p, p, p, None, 10, 64, 100, 9, p, None, None) == -2
     # 3 million rows of d = 8 would need 48 MB of the library's 32 MiB array
     assert f(p, p, p, None, 3_000_000, 8, 1000, 1, p, None, None) == -2
-    assert b"scratch" in lib.hdl_last_error()
+    assert b"scratch" in lib.hdl_last_hip_error()

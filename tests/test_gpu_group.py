@@ -183,6 +183,40 @@ def test_group_construction_full_size(hdl):
     assert pre.any() and np.all(gs[pre] == 0.0)
 
 
+def test_policy_loss_grad_token_level_mean_on_device(hdl):
+    # scale=None: the library counts the trained tokens on the device (in
+    # the mask, of a known trajectory, at or after the trajectory's start)
+    # and divides by that count, as the oracle's token-level mean does
+    rng = np.random.default_rng(12)
+    n_traj, n = 40, 70001
+    adv = rng.normal(size=n_traj).astype(np.float32)
+    traj = rng.integers(-2, n_traj + 2, n).astype(np.int32)
+    lo_ = (rng.normal(size=n) * 0.5 - 2).astype(np.float32)
+    ln = (lo_ + rng.normal(size=n) * 0.3).astype(np.float32)
+    mask = (rng.random(n) < 0.7).astype(np.uint8)
+    pos = (np.arange(n) % 4000).astype(np.int32)
+    start = rng.integers(0, 3000, n_traj).astype(np.int32)
+    cnt = torch.full((1,), -5, dtype=torch.int64, device="cuda")
+    for args in ((_t(pos), _t(start)), (None, None)):   # with and without the suffix rule
+        g, l = hdl.policy_loss_grad(_t(adv), _t(traj), _t(ln), _t(lo_), loss_mask=_t(mask), pos=args[0],
+                                    start=args[1], n_trained=cnt)
+        torch.cuda.synchronize()
+        p_, s_ = (pos, start) if args[0] is not None else (None, None)
+        want_n = O.trained_tokens(traj, n_traj, mask, p_, s_)
+        assert int(cnt.item()) == want_n
+        og, ol = O.policy_loss_grad(adv, traj, ln, lo_, mask, p_, s_, 0.2, 0.28, None)
+        g, l = g.cpu().double().numpy(), l.cpu().double().numpy()
+        r = np.exp(ln.astype(np.float64) - lo_.astype(np.float64))
+        ok = ~((np.abs(r - 0.8) < 1e-5) | (np.abs(r - 1.28) < 1e-5))
+        assert np.allclose(g[ok], og[ok], rtol=1e-5, atol=1e-14)
+        assert np.allclose(l[ok], ol[ok], rtol=1e-5, atol=1e-14)
+    # nothing trained: count 0, every factor 0
+    g, _ = hdl.policy_loss_grad(_t(adv), _t(traj), _t(ln), _t(lo_), loss_mask=_t(np.zeros(n, np.uint8)),
+                                n_trained=cnt)
+    torch.cuda.synchronize()
+    assert int(cnt.item()) == 0 and torch.all(g == 0)
+
+
 def test_policy_loss_grad_tail_and_unaligned(hdl):
     # 1001 tokens: the four-per-thread path with a ragged tail; the same data
     # as views one element into their buffers (not 16-byte aligned): the

@@ -57,7 +57,7 @@ def _run_workspace(lib, H, W, y, m):
     lse = torch.full((n,), float("nan"), device="cuda")
     st = lib.hdl_token_logprobs(H.data_ptr(), W.data_ptr(), y.data_ptr(), m.data_ptr(), n, d, V, HDL_BF16,
                                 logp.data_ptr(), lse.data_ptr(), ws.data_ptr(), nbytes, _stream())
-    assert st == 0, lib.hdl_last_error()
+    assert st == 0, lib.hdl_last_hip_error()
     return logp, lse
 
 
@@ -68,7 +68,7 @@ def _run_noalloc(lib, H, W, y, m):
     lse = torch.full((n,), float("nan"), device="cuda")
     st = lib.hdl_token_logprobs_noalloc(H.data_ptr(), W.data_ptr(), y.data_ptr(), m.data_ptr(), n, d, V,
                                         HDL_BF16, logp.data_ptr(), lse.data_ptr(), _stream())
-    assert st == 0, lib.hdl_last_error()
+    assert st == 0, lib.hdl_last_hip_error()
     return logp, lse
 
 
@@ -116,5 +116,5 @@ def test_noalloc_rejects_calls_beyond_the_array(lib):
     st = lib.hdl_token_logprobs_noalloc(H.data_ptr(), W.data_ptr(), y.data_ptr(), None, n, d, V, HDL_BF16,
                                         logp.data_ptr(), None, _stream())
     torch.cuda.synchronize()
-    assert st == -2 and b"scratch" in lib.hdl_last_error()
+    assert st == -2 and b"scratch" in lib.hdl_last_hip_error()
     assert torch.all(logp == 7.0)
