@@ -10,9 +10,11 @@
 // order like the floats (sign-magnitude flipped to an unsigned order, -0
 // folded onto +0).  The k largest s are found by a radix select on the
 // keys: four 8-bit digits, most
-// significant first, each resolved from an LDS histogram.  That yields the
-// threshold score S and how many positions at exactly S are needed; those
-// are the lowest-indexed ties (a scan in position order).  The kk <= 1024
+// significant first, each resolved from an LDS histogram (the first one
+// built while the keys are staged).  That yields the threshold score S and
+// how many positions at exactly S are needed; those are the lowest-indexed
+// ties, found in one ordered pass in which every thread owns a contiguous
+// range of positions.  The kk <= 1024
 // winners are then sorted by the composite key (s, ~t) with a bitonic sort
 // in LDS, giving the order (s descending, t ascending).
 //
@@ -146,17 +148,24 @@ __global__ __launch_bounds__(kThreads) void select_kernel(const float* __restric
   const int64_t t_hi = r_hi ? r_hi[r] : T - 1;
 
   // ---- eligibility count (and the optional signed delta) -----------------
+  // A staged root also gets the histogram of its keys' top digit here, the
+  // first radix pass's, so that pass needs no sweep of its own.
   const bool staged = T <= kStageMax;
+  for (int i = tid; i < 256; i += kThreads) sh.hist[i] = 0;
+  __syncthreads();
   int c = 0;
   for (int64_t t = tid; t < T; t += kThreads) {
     const Pos p = load_pos<VALUES>(lo, lh, mask, base, t);
     if (delta_out) delta_out[base + t] = p.delta;
     const bool cand = p.elig && t >= t_lo && t <= t_hi;
-    if (staged) sh.staged[t] = cand ? p.key : 0u;
+    if (staged) {
+      sh.staged[t] = cand ? p.key : 0u;
+      if (cand) atomicAdd(&sh.hist[p.key >> 24], 1);
+    }
     c += cand ? 1 : 0;
   }
   int n_elig;
-  block_excl_scan(c, &n_elig, sh);
+  block_excl_scan(c, &n_elig, sh);   // (its barriers also publish the histogram)
   const int kk = n_elig < pool ? n_elig : pool;
 
   if (kk > 0) {
@@ -164,13 +173,15 @@ __global__ __launch_bounds__(kThreads) void select_kernel(const float* __restric
     unsigned prefix = 0, pmask = 0;
     int rank = kk;   // rank of the threshold among positions matching prefix
     for (int shift = 24; shift >= 0; shift -= 8) {
-      for (int i = tid; i < 256; i += kThreads) sh.hist[i] = 0;
-      __syncthreads();
-      for (int64_t t = tid; t < T; t += kThreads) {
-        const unsigned key = cand_key<VALUES>(sh, staged, lo, lh, mask, base, t, t_lo, t_hi);
-        if (key != 0u && (key & pmask) == prefix) atomicAdd(&sh.hist[(key >> shift) & 255], 1);
+      if (!(staged && shift == 24)) {
+        for (int i = tid; i < 256; i += kThreads) sh.hist[i] = 0;
+        __syncthreads();
+        for (int64_t t = tid; t < T; t += kThreads) {
+          const unsigned key = cand_key<VALUES>(sh, staged, lo, lh, mask, base, t, t_lo, t_hi);
+          if (key != 0u && (key & pmask) == prefix) atomicAdd(&sh.hist[(key >> shift) & 255], 1);
+        }
+        __syncthreads();
       }
-      __syncthreads();
       // Inclusive scan over bins from the top digit down; the bin in which
       // the running count reaches `rank` holds the threshold.
       const int h = (tid < 256) ? sh.hist[255 - tid] : 0;
@@ -190,23 +201,41 @@ __global__ __launch_bounds__(kThreads) void select_kernel(const float* __restric
     const int need_ties = rank;    // positions scoring exactly thr to take
 
     // ---- collect: all above the threshold, then the lowest-indexed ties ---
-    int ties_before = 0, filled = 0;
-    for (int64_t t0 = 0; t0 < T; t0 += kThreads) {
-      const int64_t t = t0 + tid;
-      Pos p;
-      p.key = t < T ? cand_key<VALUES>(sh, staged, lo, lh, mask, base, t, t_lo, t_hi) : 0u;
-      p.elig = p.key != 0u;
-      const bool eq = p.elig && p.key == thr;
-      int n_eq;
-      const int tie_rank = ties_before + block_excl_scan(eq ? 1 : 0, &n_eq, sh);
-      const bool take = p.elig && (p.key > thr || (eq && tie_rank < need_ties));
-      int n_take;
-      const int slot = filled + block_excl_scan(take ? 1 : 0, &n_take, sh);
-      if (take && slot < kThreads)
-        sh.keys[slot] = (static_cast<unsigned long long>(p.key) << 32) |
-                        static_cast<unsigned long long>(0xFFFFFFFFu - static_cast<unsigned>(t));
-      ties_before += n_eq;
-      filled += n_take;
+    // Thread i owns the contiguous positions [i per, (i + 1) per): one scan
+    // of the per-thread tie counts gives every thread the ties at lower
+    // positions, one scan of the per-thread takes gives its output slots.
+    const int64_t per = (T + kThreads - 1) / kThreads;
+    const int64_t t_beg = tid * per;
+    const int64_t t_end = t_beg + per < T ? t_beg + per : T;
+    int my_eq = 0;
+    for (int64_t t = t_beg; t < t_end; ++t)
+      my_eq += cand_key<VALUES>(sh, staged, lo, lh, mask, base, t, t_lo, t_hi) == thr ? 1 : 0;
+    int n_eq_all;
+    const int eq_before = block_excl_scan(my_eq, &n_eq_all, sh);
+    int my_take = 0;
+    {
+      int eq_seen = eq_before;
+      for (int64_t t = t_beg; t < t_end; ++t) {
+        const unsigned key = cand_key<VALUES>(sh, staged, lo, lh, mask, base, t, t_lo, t_hi);
+        if (key > thr) ++my_take;
+        else if (key == thr && key != 0u) my_take += (eq_seen++ < need_ties) ? 1 : 0;
+      }
+    }
+    int n_take_all;
+    int slot = block_excl_scan(my_take, &n_take_all, sh);
+    {
+      int eq_seen = eq_before;
+      for (int64_t t = t_beg; t < t_end; ++t) {
+        const unsigned key = cand_key<VALUES>(sh, staged, lo, lh, mask, base, t, t_lo, t_hi);
+        bool take = key > thr;
+        if (key == thr && key != 0u) take = eq_seen++ < need_ties;
+        if (take) {
+          if (slot < kThreads)
+            sh.keys[slot] = (static_cast<unsigned long long>(key) << 32) |
+                            static_cast<unsigned long long>(0xFFFFFFFFu - static_cast<unsigned>(t));
+          ++slot;
+        }
+      }
     }
     __syncthreads();
 
