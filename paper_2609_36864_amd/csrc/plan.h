@@ -15,7 +15,7 @@ namespace hdl {
 // Fused lm-head tile geometry (see lmhead_logprob.hip).
 constexpr int kTileV = 256;              // vocabulary rows per workgroup tile
 constexpr int kTileN = 256;              // token rows per workgroup tile
-constexpr int kGroupRT = 8;              // row tiles per per-XCD launch group
+constexpr int kGroupRT = 4;              // row tiles per per-XCD launch group
 constexpr int kGroupCH = 32 / kGroupRT;  // vocabulary chunks per per-XCD launch group
 constexpr int kNumXcd = 8;               // XCDs per MI355X; workgroups go round-robin
 constexpr int kCountBlockRows = 4096;    // rows per block of the compaction's count pass
