@@ -89,3 +89,66 @@ def test_transposed_reads_are_bank_conflict_free():
                                 for b in range(a, a + 8, 4):
                                     bank = (b % width) // 4
                                     assert seen.setdefault(bank, b) == b, (slot_fn.__name__, width, kk, m0, j)
+
+
+# ---- the fused lm-head kernel's 16 x 16 x 32 fragment reads ---------------
+# A K-slice tile holds 256 rows of 8 sixteen-byte chunks (128 bytes), chunk
+# c of row r at slot 8 r + (c ^ row_xor(r)).  Fragment lane l reads row
+# R + (l mod 16) (R a multiple of 16) and chunk 4 ks + sigma(l div 16).  The
+# counters show a ds_read_b128 serving lanes i..i+7 together with lanes
+# i+32..i+39 (i = 0, 8, 16, 24) from 64 four-byte banks; under that model
+# sigma = (0, 2, 1, 3) is conflict-free and the identity is not (it collides
+# two-way in every pass, as the 4-per-read SQ_LDS_BANK_CONFLICT count of the
+# identity layout said).  The same model leaves the round-1 32 x 32 reads
+# (lane l: row l mod 32, chunk 2 kk + l div 32) conflict-free, as measured.
+
+
+def row_xor(r):
+    return (r & 7) ^ ((r >> 3) & 1)
+
+
+def frag_slot(R, ks, lane, sigma):
+    r = R + (lane & 15)
+    c = 4 * ks + sigma[lane >> 4]
+    return 8 * r + (c ^ row_xor(r))
+
+
+def frag32_slot(R, kk, lane):
+    r = R + (lane & 31)
+    c = 2 * kk + (lane >> 5)
+    return 8 * r + (c ^ row_xor(r))
+
+
+def pass_conflicts(slots):
+    """Two-way-or-worse bank collisions in the passes of one ds_read_b128."""
+    worst = 1
+    for i in range(0, 32, 8):
+        lanes = list(range(i, i + 8)) + list(range(i + 32, i + 40))
+        banks = {}
+        for l in lanes:
+            base = (slots[l] * 16 % 256) // 4
+            for b in range(base, base + 4):
+                banks[b] = banks.get(b, 0) + 1
+        worst = max(worst, max(banks.values()))
+    return worst
+
+
+def test_fused_fragment_reads_cover_the_fragment():
+    # every lane group reads a different chunk of the same 16 rows: together
+    # the 64 lanes read 16 rows x 4 chunks of the K-step exactly once
+    sigma = (0, 2, 1, 3)
+    for R in range(0, 256, 16):
+        for ks in range(2):
+            got = sorted(frag_slot(R, ks, l, sigma) for l in range(64))
+            want = sorted(8 * (R + a) + ((4 * ks + c) ^ row_xor(R + a)) for a in range(16) for c in range(4))
+            assert got == want
+
+
+def test_fused_fragment_reads_are_bank_conflict_free():
+    for R in range(0, 256, 16):
+        for ks in range(2):
+            assert pass_conflicts([frag_slot(R, ks, l, (0, 2, 1, 3)) for l in range(64)]) == 1
+            assert pass_conflicts([frag_slot(R, ks, l, (0, 1, 2, 3)) for l in range(64)]) == 2
+    for R in range(0, 256, 32):
+        for kk in range(4):
+            assert pass_conflicts([frag32_slot(R, kk, l) for l in range(64)]) == 1
