@@ -50,8 +50,8 @@ def log(msg: str) -> None:
     print(f"[bench] {msg}", file=sys.stderr, flush=True)
 
 
-# Sources the fused kernel is compiled from.
-KERNEL_SOURCES = ("lmhead_logprob.hip", "tile_common.h", "hdl_internal.h")
+# Sources the fused kernel and its launch (work-item order, chunking) come from.
+KERNEL_SOURCES = ("lmhead_logprob.hip", "tile_common.h", "hdl_internal.h", "plan.h")
 
 
 def kernel_source_sha() -> str:
