@@ -156,11 +156,13 @@ __global__ void clear_count_kernel(unsigned long long* n) { *n = 0ull; }
 // (VEC = 4 under the alignment policy_grad_kernel's vector path needs), then
 // one integer atomic add per workgroup -- exact, so the order does not
 // matter, and few enough workgroups that the adds to one address do not
-// queue up.
+// queue up.  1024-thread workgroups keep 32 waves per CU loading with only
+// 512 atomics.
 constexpr int kCountBlocks = 512;
+constexpr int kCountThreads = 1024;
 
 template <int VEC>
-__global__ __launch_bounds__(256) void count_trained_kernel(PolicyGradArgs p) {
+__global__ __launch_bounds__(kCountThreads) void count_trained_kernel(PolicyGradArgs p) {
   unsigned c = 0;
   const int64_t stride = static_cast<int64_t>(gridDim.x) * blockDim.x * VEC;
   for (int64_t n0 = (static_cast<int64_t>(blockIdx.x) * blockDim.x + threadIdx.x) * VEC; n0 < p.n_tokens;
@@ -177,12 +179,13 @@ __global__ __launch_bounds__(256) void count_trained_kernel(PolicyGradArgs p) {
         c += trained(p, p.traj[n], p.pos ? p.pos[n] : 0, p.loss_mask ? p.loss_mask[n] : 1);
     }
   }
-  __shared__ unsigned part[4];
+  __shared__ unsigned part[kCountThreads / 64];
   for (int o = 32; o > 0; o >>= 1) c += __shfl_xor(c, o);
   if ((threadIdx.x & 63) == 0) part[threadIdx.x >> 6] = c;
   __syncthreads();
   if (threadIdx.x == 0) {
-    const unsigned long long t = static_cast<unsigned long long>(part[0]) + part[1] + part[2] + part[3];
+    unsigned long long t = 0;
+    for (int w = 0; w < kCountThreads / 64; ++w) t += part[w];
     if (t) atomicAdd(p.n_trained, t);
   }
 }
@@ -222,11 +225,13 @@ hipError_t launch_policy_grad(const float* adv, const int32_t* traj, const int32
     hipLaunchKernelGGL(clear_count_kernel, dim3(1), dim3(1), 0, stream, a.n_trained);
     hipError_t e = hipGetLastError();
     if (e != hipSuccess) return e;
-    const unsigned cb = static_cast<unsigned>(blocks < kCountBlocks ? blocks : kCountBlocks);
+    const int64_t per_block = static_cast<int64_t>(kCountThreads) * (vec ? 4 : 1);
+    const int64_t need = (n_tokens + per_block - 1) / per_block;
+    const unsigned cb = static_cast<unsigned>(need < kCountBlocks ? need : kCountBlocks);
     if (vec)
-      hipLaunchKernelGGL(count_trained_kernel<4>, dim3(cb), dim3(256), 0, stream, a);
+      hipLaunchKernelGGL(count_trained_kernel<4>, dim3(cb), dim3(kCountThreads), 0, stream, a);
     else
-      hipLaunchKernelGGL(count_trained_kernel<1>, dim3(cb), dim3(256), 0, stream, a);
+      hipLaunchKernelGGL(count_trained_kernel<1>, dim3(cb), dim3(kCountThreads), 0, stream, a);
     if ((e = hipGetLastError()) != hipSuccess) return e;
   }
   if (vec)

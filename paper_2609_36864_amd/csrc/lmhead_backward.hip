@@ -34,56 +34,77 @@ constexpr int kGemmSliceK = 8 * kChunks;   // bf16 elements per K-slice
 constexpr int kKRowChunks = kTileV * 2 / 16;
 static_assert(kGemmSliceK * kKRowChunks == kSlots, "K-row slice must fill one operand stage");
 static_assert(2 * kKRowChunks == 64, "one DMA block must hold two stored K rows");
+static_assert(kKSteps * 32 == kGemmSliceK, "a K-slice is two K-steps of 32");
 
 typedef short i16x4_t __attribute__((ext_vector_type(4)));
 
-// XOR pattern of the 16-byte chunks of K-row r.  A transposing read by 16
-// lanes touches 32 bytes (two chunks) in each of 4 consecutive rows, and 32
-// lanes touch 64 bytes in each of those rows; with 512-byte rows every row
-// starts on the same bank, so the pattern must give the 4 rows distinct
-// 32-byte bank positions within 128 bytes (bits 1-2 of the chunk index) and
-// distinct 64-byte positions within 256 bytes (bits 2-3): (j0, j1) = the two
-// low bits of r map to bits (2, 1) and bit 3 takes j0 ^ j1.
-__device__ __forceinline__ int krow_xor(int r) {
-  const int j0 = r & 1, j1 = (r >> 1) & 1;
-  return 2 * j1 + 4 * j0 + 8 * (j0 ^ j1);
-}
+// Operands whose stored rows run along K (W in dH, G in dW) are turned into
+// MFMA fragments by gfx950's transposing read ds_read_b64_tr_b16: within
+// each 16-lane group, lane i receives element i mod 4 of the 8-byte pieces
+// addressed by lanes i/4, i/4 + 4, i/4 + 8 and i/4 + 12.  For the fragment
+// of 16 columns m0 .. m0+15 at K-step ks, lane a of lane group g addresses
+// stored K row 32 ks + 8 frag_chunk(g) + 4 j + a/4 at columns
+// m0 + 4 (a mod 4) .. +3 (read j = 0, 1): lane a then holds column m0 + a,
+// K values 8 frag_chunk(g) + 4 j + 0..3 of the K-step, as the MFMA wants.
+// A read touches 4 rows x 32 bytes per lane group; the groups read rows
+// whose bits 3-4 are (0, 0), (0, 1), (1, 0), (1, 1) (g = 0, 1, 2, 3).
 
-// Chunk-major tiles in the K-row role: stored row r of the slice in chunk
-// c sits at slot c * 64 + (r ^ cm_xor(c)).  A transposing read by 32 lanes
-// touches 4 consecutive rows (64 bytes) in each of 4 consecutive chunks,
-// which start 1 KB apart (same bank): XOR-ing bits 2-3 of the row with the
-// chunk's two low bits puts the 4 segments in distinct 64-byte bank ranges
-// (and any 2 consecutive chunks in distinct 32-byte ranges of 128 bytes).
-__device__ __forceinline__ int cm_xor(int c) { return 4 * (c & 3); }
+// XOR pattern of the 16-byte chunks of K row r (512-byte rows, so every
+// row starts on the same bank): the 32-byte pieces that 4 rows x 4 groups
+// read must fall in distinct 32-byte bank positions of 128 bytes (one
+// group) and of 256 bytes (two groups, whichever two the LDS serves
+// together): bits 1-3 of the chunk take r mod 4 and bit 3 ^ bit 4 of r.
+__device__ __forceinline__ int krow_xor(int r) { return 2 * ((r & 3) | ((((r >> 3) ^ (r >> 4)) & 1) << 2)); }
+
+// Chunk-major tiles in the K-row role: stored row r of the slice in chunk c
+// sits at slot c * 64 + (r ^ cm_xor(c, r)) (1 KB per chunk, so chunks start
+// on the same bank).  A lane group reads 4 rows of 2 chunks (c even, c + 1):
+// bit 2 of the row takes c mod 2, bit 3 takes bit 4 of the row, so 8 pieces
+// of one group and 16 of any two groups land in distinct 16-byte positions.
+// Only bits 2-3 change, so the pattern is its own inverse.
+__device__ __forceinline__ int cm_xor(int c, int r) { return (4 * (c & 1)) ^ (8 * ((r >> 4) & 1)); }
 
 // Per-lane DMA and fragment addressing of one operand of the tile, by
 // stored layout (GemmArgs::a_layout / b_layout):
 //   kLayoutKRow   X(i, k) at k * ld + i: row k holds the tile's columns;
-//                 LDS slot of (row r, chunk c) = r * 32 + (c ^ krow_xor(r)).
+//                 LDS slot of (K row r, chunk c) = r * 32 + (c ^ krow_xor(r)).
 //   kLayoutCmRow  X(i, k) at ((k / 8) * ld + i) * 8 + k % 8 (chunk-major,
 //                 K split into chunks); LDS slot of (row i, chunk c) =
-//                 c * 256 + i, read with plain 16-byte loads.
+//                 c * 256 + i, so that each DMA block reads 1 KB contiguous
+//                 (with the fused kernel's row-major tiles a DMA block would
+//                 read 8 runs of 128 bytes from 8 chunk planes a power of
+//                 two apart, which ran the GEMMs 13 % slower); read with
+//                 plain 16-byte loads.  Lane groups g and g + 2 (served
+//                 together) read chunks 2 m and 2 m + 1 of the same rows,
+//                 4 KB apart: 0 bank conflicts measured, as for the 32-row
+//                 fragments of the same layout.
 //   kLayoutCmKRow X(i, k) at ((i / 8) * ld + k) * 8 + i % 8 (chunk-major,
 //                 the tile's columns split into chunks); LDS slot as for
 //                 cm_xor above, read with transposing loads.
 // In every case one DMA block of 64 lanes fills 64 consecutive LDS slots,
-// and a K-slice fills 2048 slots (32 KB).
-template <int LAY>
+// and a K-slice fills 2048 slots (32 KB).  NBLK: the operand's 16-column
+// fragments per wave (kVB as A, kTB as B).
+template <int LAY, int NBLK>
 struct Operand {
+  static constexpr int kFragOffs = LAY == kLayoutKRow ? NBLK : 2;
   uint32_t off[kBlocksPerWave];   // per-lane byte offset of each DMA block (kLayoutCmRow: final)
   uint64_t tile;                  // uniform base of the tile
   int64_t ld;                     // elements between stored rows (chunk-major: rows per chunk plane)
   int64_t krows;                  // stored K rows (K-row roles)
-  uint32_t frag_lo[4], frag_hi[4];   // transposing reads: per-lane LDS byte offset of each 32-wide block
+  // per-lane LDS offsets of the fragment reads: kLayoutCmRow: 16-byte slot
+  // per K-step; kLayoutKRow: byte offset per fragment; kLayoutCmKRow: byte
+  // offset per read j
+  uint32_t frag_off[kFragOffs];
 
   // t0: first column (tile index) of the tile; rows / cols: valid extent
-  // of that index (row role) or stored columns (K-row roles; a multiple of 8).
+  // of that index (row role) or stored columns (K-row roles; a multiple of
+  // 8); fbase: the wave's first column within the tile.
   __device__ __forceinline__ void init(const void* ptr, int64_t ld_, int64_t t0, int64_t rows, int64_t cols,
-                                       int64_t krows_, int wave, int lane, int nblk, int blk0) {
+                                       int64_t krows_, int wave, int lane, int fbase) {
     ld = ld_;
     krows = krows_;
-    const int a = lane & 15, gi = (lane >> 4) & 1, half = lane >> 5;
+    const int a = lane & 15, grp = lane >> 4;
+    const int r0 = 8 * frag_chunk(grp) + (a >> 2);   // fragment K row of read j = 0 at K-step 0
     if (LAY == kLayoutKRow) {
       tile = reinterpret_cast<uint64_t>(ptr) + static_cast<uint64_t>(t0 * 2);
 #pragma unroll
@@ -94,14 +115,12 @@ struct Operand {
         c = c < cols - 8 ? c : cols - 8;
         off[i] = static_cast<uint32_t>((c - t0) * 2);   // + row * ld * 2 at issue
       }
-      // lane l of a 16-lane group reads stored row 4 j + l / 4 (j: which half
-      // of the 8 K values) at columns 4 (l % 4) .. +3 of its group's 16
-      // columns; lanes 32-63 take K values 8-15 of the sub-step
+      // krow_xor of the rows read depends on bits 0, 1, 3, 4 only: the same
+      // for both reads and both K-steps
 #pragma unroll
-      for (int bk = 0; bk < nblk; ++bk) {
-        const int c = (((blk0 + bk * 32) >> 3) + 2 * gi + ((a & 3) >> 1)) ^ krow_xor(a >> 2);
-        frag_lo[bk] = static_cast<uint32_t>(((a >> 2) + 8 * half) * (kKRowChunks * 16) + c * 16 + (a & 1) * 8);
-        frag_hi[bk] = frag_lo[bk] + 4 * kKRowChunks * 16;
+      for (int b = 0; b < NBLK; ++b) {
+        const int c = ((fbase + 16 * b) >> 3) + ((a & 3) >> 1);
+        frag_off[b] = static_cast<uint32_t>((r0 * kKRowChunks + (c ^ krow_xor(r0))) * 16 + (a & 1) * 8);
       }
     } else if (LAY == kLayoutCmRow) {
       tile = reinterpret_cast<uint64_t>(ptr) + static_cast<uint64_t>(t0 * 16);
@@ -112,22 +131,28 @@ struct Operand {
         row = row < rows ? row : rows - 1;
         off[i] = static_cast<uint32_t>((wave * ld + (row - t0)) * 16);
       }
+#pragma unroll
+      for (int ks = 0; ks < 2; ++ks)
+        frag_off[ks] = static_cast<uint32_t>((4 * ks + frag_chunk(grp)) * kTileV + fbase + a);
     } else {
       const int64_t c0 = t0 / 8;
       tile = reinterpret_cast<uint64_t>(ptr) + static_cast<uint64_t>(c0 * ld * 16);
 #pragma unroll
       for (int i = 0; i < kBlocksPerWave; ++i) {
-        // block wave*4 + i = chunk c = wave * 4 + i, slot lane = row lane ^ cm_xor(c)
+        // block wave * 4 + i = chunk c = wave * 4 + i, slot lane = row lane ^ cm_xor(c, lane)
         int64_t c = c0 + wave * kBlocksPerWave + i;
         c = c < cols / 8 - 1 ? c : cols / 8 - 1;
         off[i] = static_cast<uint32_t>((c - c0) * ld * 16);   // + row * 16 at issue
       }
+      // chunk of the lane's columns: fbase / 8 + 2 b + (a mod 4) / 2, whose
+      // parity is that of (a mod 4) / 2; bit 4 of the rows read is
+      // frag_chunk(g) / 2 for both reads and both K-steps
+      const int cpar = (a & 3) >> 1;
 #pragma unroll
-      for (int bk = 0; bk < nblk; ++bk) {
-        const int c = ((blk0 + bk * 32) >> 3) + 2 * gi + ((a & 3) >> 1);
-        const int r = 8 * half + (a >> 2);   // bits 2-3: 0 / half; + 4 j for the second read
-        frag_lo[bk] = static_cast<uint32_t>((c * 64 + (r ^ cm_xor(c))) * 16 + (a & 1) * 8);
-        frag_hi[bk] = static_cast<uint32_t>((c * 64 + ((r + 4) ^ cm_xor(c))) * 16 + (a & 1) * 8);
+      for (int j = 0; j < 2; ++j) {
+        const int r = r0 + 4 * j;
+        frag_off[j] = static_cast<uint32_t>(((fbase >> 3) + cpar) * 64 * 16 + (r ^ cm_xor(cpar, r)) * 16 +
+                                            (a & 1) * 8);
       }
     }
   }
@@ -146,23 +171,30 @@ struct Operand {
   // per-lane offset of DMA block i of a K-slice whose last stored row is rmax
   __device__ __forceinline__ uint32_t block_off(int i, int rmax, int wave, int lane) const {
     if (LAY == kLayoutCmRow) return off[i];
-    const int r = LAY == kLayoutKRow ? 2 * (wave * kBlocksPerWave + i) + (lane >> 5) : lane ^ (4 * i);
+    const int r = LAY == kLayoutKRow ? 2 * (wave * kBlocksPerWave + i) + (lane >> 5)
+                                     : lane ^ cm_xor(wave * kBlocksPerWave + i, lane);
     const int rr = r < rmax ? r : rmax;
     return LAY == kLayoutKRow ? static_cast<uint32_t>(rr) * static_cast<uint32_t>(ld * 2) + off[i]
                               : static_cast<uint32_t>(rr) * 16u + off[i];
   }
-  // the 16-byte MFMA fragment of 32-wide block bk (first column mbase of the
-  // tile) for sub-step kk: 8 consecutive K values of column mbase + lane % 32
-  __device__ __forceinline__ uint4 frag(const uint4* stage_op, int bk, int mbase, int kk, int lane) const {
-    if (LAY == kLayoutCmRow) return stage_op[(kk * 2 + (lane >> 5)) * kTileV + mbase + (lane & 31)];
+  // The MFMA fragment of 16-column block b of the wave at K-step ks.
+  __device__ __forceinline__ uint4 frag(const uint4* stage_op, int b, int ks) const {
+    if (LAY == kLayoutCmRow) return stage_op[frag_off[ks] + b * 16];
+    typedef __attribute__((address_space(3))) char lds_char;
+    const lds_char* base = (const lds_char*)((const __attribute__((address_space(3))) uint4*)stage_op);
     typedef __attribute__((address_space(3))) i16x4_t lds_i16x4;
-    const char __attribute__((address_space(3)))* base =
-        (const char __attribute__((address_space(3)))*)(
-            (const __attribute__((address_space(3))) uint4*)stage_op);
-    // sub-step kk covers stored rows 16 kk .. 16 kk + 15 (untouched by the XOR patterns)
-    const uint32_t ks = static_cast<uint32_t>(kk * 16 * (LAY == kLayoutKRow ? kKRowChunks * 16 : 16));
-    const i16x4_t lo = __builtin_amdgcn_ds_read_tr16_b64_v4i16((lds_i16x4*)(base + frag_lo[bk] + ks));
-    const i16x4_t hi = __builtin_amdgcn_ds_read_tr16_b64_v4i16((lds_i16x4*)(base + frag_hi[bk] + ks));
+    uint32_t o0, o1;
+    if (LAY == kLayoutKRow) {
+      // K-step ks: rows + 32 ks; read 1: rows + 4
+      o0 = frag_off[b] + ks * 32 * kKRowChunks * 16;
+      o1 = o0 + 4 * kKRowChunks * 16;
+    } else {
+      // fragment b: chunks + 2 b; K-step ks: rows + 32 ks
+      o0 = frag_off[0] + b * 2 * 64 * 16 + ks * 32 * 16;
+      o1 = frag_off[1] + b * 2 * 64 * 16 + ks * 32 * 16;
+    }
+    const i16x4_t lo = __builtin_amdgcn_ds_read_tr16_b64_v4i16((lds_i16x4*)(base + o0));
+    const i16x4_t hi = __builtin_amdgcn_ds_read_tr16_b64_v4i16((lds_i16x4*)(base + o1));
     const uint2 l = __builtin_bit_cast(uint2, lo), h = __builtin_bit_cast(uint2, hi);
     return make_uint4(l.x, l.y, h.x, h.y);
   }
@@ -171,12 +203,12 @@ struct Operand {
 // C[s][m][n] (=|+=) sum_k A(m, k) B(n, k) over the K range of split s, for
 // one 256 x 256 tile of C per workgroup.  Same data path as the fused
 // kernel: K-slices of 64 K values stream into a 2-stage LDS ring by direct
-// DMA; eight waves each own 128 x 64 of the tile as 4 x 2 MFMA blocks.
+// DMA; eight waves each own 128 x 64 of the tile as 8 x 4 blocks of
+// v_mfma_f32_16x16x32_bf16, with the fused kernel's quarter schedule.
 // LA / LB: stored layouts of A and B (see Operand).
 template <int LA, int LB>
 __global__ __launch_bounds__(kThreads, 1) void gemm_kernel(GemmArgs p) {
-  using M = Mma<true>;
-  static_assert(kWaves == 8 && kNB == 2, "8-wave tile layout assumed");
+  using M = Mma16<true>;
   __shared__ uint4 lds[kStages][2][kSlots];   // [stage][0 = A, 1 = B]
 
   const int tid = threadIdx.x;
@@ -184,8 +216,8 @@ __global__ __launch_bounds__(kThreads, 1) void gemm_kernel(GemmArgs p) {
   const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);
   const int wm = wave & 1;
   const int wn = wave >> 1;
-  const int half = lane >> 5;
-  const int col = lane & 31;
+  const int r16 = lane & 15;
+  const int grp = lane >> 4;
 
   // ---- work item: XCD-aware (m-tile, n-tile, split) ----------------------
   // The j-th workgroup of an XCD belongs to launch group j / 32 of that XCD;
@@ -193,14 +225,14 @@ __global__ __launch_bounds__(kThreads, 1) void gemm_kernel(GemmArgs p) {
   const int64_t b = blockIdx.x;
   const int64_t xcd = b % kNumXcd;
   const int64_t j = b / kNumXcd;
-  const int64_t grp = (j / (p.gm * p.gn)) * kNumXcd + xcd;
+  const int64_t grp_id = (j / (p.gm * p.gn)) * kNumXcd + xcd;
   const int64_t loc = j % (p.gm * p.gn);
   const int64_t n_gm = (p.tiles_m + p.gm - 1) / p.gm;
   const int64_t n_gn = (p.tiles_n + p.gn - 1) / p.gn;
   // (the runtime divisions run on the vector ALU; readfirstlane puts the
   // wave-uniform results back in scalar registers for the DMA base)
-  const int64_t split = __builtin_amdgcn_readfirstlane(static_cast<int>(grp / (n_gm * n_gn)));
-  const int64_t rem = grp % (n_gm * n_gn);
+  const int64_t split = __builtin_amdgcn_readfirstlane(static_cast<int>(grp_id / (n_gm * n_gn)));
+  const int64_t rem = grp_id % (n_gm * n_gn);
   const int64_t tm = __builtin_amdgcn_readfirstlane(static_cast<int>((rem % n_gm) * p.gm + loc % p.gm));
   const int64_t tn = __builtin_amdgcn_readfirstlane(static_cast<int>((rem / n_gm) * p.gn + loc / p.gm));
   if (split >= p.splits || tm >= p.tiles_m || tn >= p.tiles_n) return;
@@ -219,19 +251,19 @@ __global__ __launch_bounds__(kThreads, 1) void gemm_kernel(GemmArgs p) {
   const int n_iter = k1 > k0 ? static_cast<int>((k1 - k0) / kGemmSliceK) : 0;
   if (n_iter == 0 && p.beta) return;   // nothing to add
 
-  f32x16_t acc[4][kNB];
+  f32x4_t acc[kVB][kTB];
 #pragma unroll
-  for (int bm = 0; bm < 4; ++bm)
+  for (int bm = 0; bm < kVB; ++bm)
 #pragma unroll
-    for (int bn = 0; bn < kNB; ++bn)
+    for (int bn = 0; bn < kTB; ++bn)
 #pragma unroll
-      for (int q = 0; q < 16; ++q) acc[bm][bn][q] = 0.f;
+      for (int q = 0; q < 4; ++q) acc[bm][bn][q] = 0.f;
 
   if (n_iter > 0) {
-    Operand<LA> A;
-    Operand<LB> B;
-    A.init(p.a, p.lda, tm * kTileV, m_valid, p.a_cols, p.a_krows, wave, lane, 4, wm * 128);
-    B.init(p.b, p.ldb, tn * kTileN, p.n, p.b_cols, p.b_krows, wave, lane, kNB, wn * kWaveN);
+    Operand<LA, kVB> A;
+    Operand<LB, kTB> B;
+    A.init(p.a, p.lda, tm * kTileV, m_valid, p.a_cols, p.a_krows, wave, lane, wm * 16 * kVB);
+    B.init(p.b, p.ldb, tn * kTileN, p.n, p.b_cols, p.b_krows, wave, lane, wn * kWaveN);
     const uint32_t lds_base = static_cast<uint32_t>(
         reinterpret_cast<size_t>((__attribute__((address_space(3))) uint4*)(&lds[0][0][0])));
     auto lds_addr = [&](int stage, int op, int block) -> uint32_t {
@@ -240,8 +272,10 @@ __global__ __launch_bounds__(kThreads, 1) void gemm_kernel(GemmArgs p) {
     };
     int issue_stage = 0, a_rmax = 0, b_rmax = 0;
     uint64_t a_slice = 0, b_slice = 0;
-    auto prep_issue = [&](int slice) {
-      issue_stage = slice % kStages;
+    // slot: the ring position (its stage); slice: the data fetched into it
+    // (they differ only for the copies of the last slice past the end)
+    auto prep_issue = [&](int slot, int slice) {
+      issue_stage = slot % kStages;
       const int64_t k = k0 + static_cast<int64_t>(slice) * kGemmSliceK;
       a_slice = A.slice_base(k);
       b_slice = B.slice_base(k);
@@ -255,66 +289,86 @@ __global__ __launch_bounds__(kThreads, 1) void gemm_kernel(GemmArgs p) {
       else
         dma16(b_slice, B.block_off(i, b_rmax, wave, lane), lds_addr(issue_stage, 1, wave * kBlocksPerWave + i));
     };
-    auto load_frags = [&](int slice, int kk, uint4 (&fa)[4], uint4 (&fb)[kNB]) {
-      const int stage = slice % kStages;
+    // the two A fragments (M blocks 2 pr, 2 pr + 1) of quarter pr of K-step ks
+    auto load_a = [&](int slice, int ks, int pr, uint4 (&dst)[2]) {
 #pragma unroll
-      for (int bm = 0; bm < 4; ++bm) fa[bm] = A.frag(lds[stage][0], bm, wm * 128 + bm * 32, kk, lane);
+      for (int jj = 0; jj < 2; ++jj) dst[jj] = A.frag(lds[slice % kStages][0], 2 * pr + jj, ks);
+    };
+    auto load_b = [&](int slice, int ks, int bn, uint4& dst) { dst = B.frag(lds[slice % kStages][1], bn, ks); };
+    auto quarter_mfma = [&](const uint4 (&fa_)[2], const uint4 (&fb_)[kTB], int pr) {
 #pragma unroll
-      for (int bn = 0; bn < kNB; ++bn) fb[bn] = B.frag(lds[stage][1], bn, wn * kWaveN + bn * 32, kk, lane);
+      for (int jj = 0; jj < 2; ++jj)
+#pragma unroll
+        for (int bn = 0; bn < kTB; ++bn) M::run(fa_[jj], fb_[bn], acc[2 * pr + jj][bn]);
     };
 
     const int n_pre = n_iter < kStages ? n_iter : kStages;
     for (int sl = 0; sl < n_pre; ++sl) {
-      prep_issue(sl);
+      prep_issue(sl, sl);
 #pragma unroll
       for (int jj = 0; jj < kDmaPerSlice; ++jj) issue_one(jj);
     }
     wait_dma(n_pre - 1);
     raw_barrier();
 
-    uint4 fa[2][4], fb[2][kNB];
-    load_frags(0, 0, fa[0], fb[0]);
+    // The fused kernel's schedule: a K-slice is 2 K-steps x 4 quarters;
+    // each quarter first reads what the next one needs (the next two A
+    // fragments, and during K-step 0 one B fragment of K-step 1), and the
+    // slice's last quarter crosses the barrier into the next slice and
+    // issues the DMA of the slice after next between its MFMAs.
+    uint4 fa[2][2], fb[2][kTB];
+    load_a(0, 0, 0, fa[0]);
+#pragma unroll
+    for (int bn = 0; bn < kTB; ++bn) load_b(0, 0, bn, fb[0][bn]);
     for (int it = 0; it < n_iter; ++it) {
 #pragma unroll
-      for (int kk = 0; kk < kSub; ++kk) {
-        const int cur = kk & 1;
-        if (kk + 1 < kSub) {
-          load_frags(it, kk + 1, fa[cur ^ 1], fb[cur ^ 1]);
-          __builtin_amdgcn_sched_barrier(0);
+      for (int pr = 0; pr < 4; ++pr) {
+        if (pr < 3) load_a(it, 0, pr + 1, fa[(pr + 1) & 1]);
+        else load_a(it, 1, 0, fa[0]);
+        load_b(it, 1, pr, fb[1][pr]);
+        __builtin_amdgcn_sched_barrier(0);
+        quarter_mfma(fa[pr & 1], fb[0], pr);
+      }
 #pragma unroll
-          for (int q = 0; q < 4 * kNB; ++q) M::run(fa[cur][q / kNB], fb[cur][q % kNB], acc[q / kNB][q % kNB]);
-        } else {
-          // Every read of slice `it` is issued: wait for slice it+1, then
-          // refill this slice's stage with slice it+kStages (past the end:
-          // the last slice again, into a stage nothing reads any more; the
-          // fragment reads of the call's last step fetch stale, unused LDS).
-          wait_dma(kStages - 2);
-          raw_barrier();
-          prep_issue(it + kStages < n_iter ? it + kStages : n_iter - 1);
-          load_frags(it + 1, 0, fa[cur ^ 1], fb[cur ^ 1]);
-          __builtin_amdgcn_sched_barrier(0);
+      for (int pr = 0; pr < 3; ++pr) {
+        load_a(it, 1, pr + 1, fa[(pr + 1) & 1]);
+        __builtin_amdgcn_sched_barrier(0);
+        quarter_mfma(fa[pr & 1], fb[1], pr);
+      }
+      // Every read of slice `it` is issued: wait for slice it+1, then refill
+      // this slice's stage with slice it+kStages (past the end: a copy of
+      // the last slice, into a stage nothing reads any more; the fragment
+      // reads of the call's last step fetch stale, unused LDS).
+      wait_dma(kStages - 2);
+      raw_barrier();
+      prep_issue(it + kStages, it + kStages < n_iter ? it + kStages : n_iter - 1);
+      load_a(it + 1, 0, 0, fa[0]);
 #pragma unroll
-          for (int q = 0; q < 4 * kNB; ++q) {
-            M::run(fa[cur][q / kNB], fb[cur][q % kNB], acc[q / kNB][q % kNB]);
-            issue_one(q);   // 8 MFMAs, 8 DMAs per slice
-          }
-        }
+      for (int bn = 0; bn < kTB; ++bn) load_b(it + 1, 0, bn, fb[0][bn]);
+      __builtin_amdgcn_sched_barrier(0);
+      constexpr int kM = 2 * kTB;   // MFMAs per quarter, one DMA after each
+      static_assert(kM == kDmaPerSlice, "one DMA per MFMA of the last quarter");
+#pragma unroll
+      for (int q = 0; q < kM; ++q) {
+        M::run(fa[1][q / kTB], fb[1][q % kTB], acc[6 + q / kTB][q % kTB]);
+        issue_one(q);
       }
     }
     wait_vmcnt<0>();
   }
 
-  // ---- store: lanes of one accumulator element cover 32 consecutive n ----
+  // ---- store: in each block, lane l holds column l mod 16 of rows
+  // 4 (l div 16) + q, so one store instruction covers 4 rows x 64 bytes ----
   float* cbase = p.c + split * p.c_split_stride;
 #pragma unroll
-  for (int bn = 0; bn < kNB; ++bn) {
-    const int64_t n = tn * kTileN + wn * kWaveN + bn * 32 + col;
+  for (int bn = 0; bn < kTB; ++bn) {
+    const int64_t n = tn * kTileN + wn * kWaveN + bn * 16 + r16;
     if (n >= p.n) continue;
 #pragma unroll
-    for (int bm = 0; bm < 4; ++bm)
+    for (int bm = 0; bm < kVB; ++bm)
 #pragma unroll
-      for (int q = 0; q < 16; ++q) {
-        const int64_t m = tm * kTileV + wm * 128 + bm * 32 + acc_row(q, half);
+      for (int q = 0; q < 4; ++q) {
+        const int64_t m = tm * kTileV + wm * 16 * kVB + bm * 16 + 4 * grp + q;
         if (m < m_valid) {
           float* dst = cbase + m * p.ldc + n;
           *dst = p.beta ? *dst + acc[bm][bn][q] : acc[bm][bn][q];

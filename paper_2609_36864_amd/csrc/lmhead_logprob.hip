@@ -19,28 +19,24 @@
 // the V-tiles of one chunk.  Eight waves per workgroup (two per SIMD, so one
 // wave's LDS reads and DMA issue overlap the other's MFMAs; the per-V-tile
 // epilogue, which both reach after the same slice, does not), each owning
-// 128 vocab x 64 tokens as a 4x2 grid of 32x32 MFMA blocks with fp32
-// accumulators.
+// 128 vocab x 64 tokens as an 8 x 4 grid of 16 x 16 MFMA blocks
+// (v_mfma_f32_16x16x32_bf16) with fp32 accumulators.
 // W is the MFMA "A" operand (vocabulary on the M axis) and the hidden states
 // are the "B" operand (tokens on the N axis), so each lane's accumulators
-// hold one token column and 64 vocabulary rows: the online max / sum-of-exp
-// update of a V-tile is entirely lane-local, and lanes and waves are merged
-// only once per work item.
+// hold 4 token columns and 32 vocabulary rows each: the online max /
+// sum-of-exp update of a V-tile is entirely lane-local, and lanes and waves
+// are merged only once per work item.
 //
 // Operands stream through LDS in K-slices of 128 bytes per row (64 bf16 or
 // 32 fp32) through a ring of 2 stages (128 KB): the next slice is in flight
 // (global -> LDS DMA, no VGPR staging) while slice i is multiplied.  16-byte
-// chunks are XOR swizzled so that the 32-row fragment reads are bank-conflict
-// free.  The DMA is issued from inline assembly (wave-uniform 64-bit base +
+// chunks are XOR swizzled and each lane group reads the chunk frag_chunk()
+// assigns it, so that the 16-row fragment reads are bank-conflict free.
+// The DMA is issued from inline assembly (wave-uniform 64-bit base +
 // per-lane 32-bit offset) and waited for with explicit vmcnt counts: the
 // compiler cannot see that a DMA into one stage does not alias the reads of
 // another, and would otherwise wait for every outstanding DMA before each LDS
 // read.
-//
-// Both operands are contiguous in K.  MFMA lane l takes row (l mod 32) and a
-// 16-byte K fragment chosen by (l div 32); A and B fragments use the same K
-// assignment, so the contraction is exact whatever order the hardware sums
-// the K values in.
 #include "tile_common.h"
 
 #include <type_traits>
@@ -77,38 +73,6 @@ __device__ __forceinline__ void combine(float& m, float& s, float& z, float& t, 
   z = fmaxf(z, z2);
 }
 
-// The MFMA shape of this kernel: v_mfma_f32_16x16x32_bf16 (fp32 inputs: four
-// v_mfma_f32_16x16x4_f32 over one 16-byte fragment).  A fragment is 16 rows
-// of one operand: lane l holds row (l mod 16) and the 16-byte chunk
-// (4 ks + sigma(l div 16)) of the K-slice (see the fragment reads), i.e. 8 bf16 (4 fp32) consecutive K
-// values; A and B fragments take the same K positions, so the contraction is
-// exact whatever order the hardware sums them in.  The 16 x 16 fp32 result
-// block sits in 4 registers per lane: column (l mod 16), rows
-// 4 (l div 16) + i.
-template <bool BF16> struct Mma16;
-
-template <> struct Mma16<true> {
-  __device__ __forceinline__ static void run(const uint4& a, const uint4& b, f32x4_t& c) {
-    c = __builtin_amdgcn_mfma_f32_16x16x32_bf16(__builtin_bit_cast(bf16x8_t, a), __builtin_bit_cast(bf16x8_t, b), c,
-                                                0, 0, 0);
-  }
-};
-
-template <> struct Mma16<false> {
-  // Four K = 4 steps; lane group g supplies K offset 4 g + j in step j, the
-  // same for both operands, so the four steps cover the fragment's 16 K values.
-  __device__ __forceinline__ static void run(const uint4& a, const uint4& b, f32x4_t& c) {
-    c = __builtin_amdgcn_mfma_f32_16x16x4f32(__uint_as_float(a.x), __uint_as_float(b.x), c, 0, 0, 0);
-    c = __builtin_amdgcn_mfma_f32_16x16x4f32(__uint_as_float(a.y), __uint_as_float(b.y), c, 0, 0, 0);
-    c = __builtin_amdgcn_mfma_f32_16x16x4f32(__uint_as_float(a.z), __uint_as_float(b.z), c, 0, 0, 0);
-    c = __builtin_amdgcn_mfma_f32_16x16x4f32(__uint_as_float(a.w), __uint_as_float(b.w), c, 0, 0, 0);
-  }
-};
-
-constexpr int kVB = 8;    // 16-row vocabulary blocks per wave (128 vocabulary rows)
-constexpr int kTB = 4;    // 16-token blocks per wave (kWaveN = 64 tokens)
-constexpr int kKSteps = kChunks / 4;   // K-steps of 4 chunks (64 bytes per row) per K-slice
-static_assert(kTB * 16 == kWaveN, "wave token span");
 static_assert(kKSteps == 2, "a K-slice is two K-steps");
 
 // KTAIL: d is not a multiple of the K-slice, so the last slice of every
@@ -238,8 +202,10 @@ __global__ __launch_bounds__(kThreads, 1) void lmhead_logprob_kernel(LmheadArgs 
   uint32_t issue_kbytes = 0;
   int issue_stage = 0;
   bool issue_tail = false;
-  auto prep_issue = [&](int slice) {
-    issue_stage = slice % kStages;
+  // slot: the ring position (its stage); slice: the data fetched into it
+  // (they differ only for the copies of the last slice past the end)
+  auto prep_issue = [&](int slot, int slice) {
+    issue_stage = slot % kStages;
     const int kt = slice % nk;
     if (kt == 0) set_w(vt0 + slice / nk);
     issue_kbytes = static_cast<uint32_t>(kt) * kSliceK * kEsz;
@@ -262,7 +228,7 @@ __global__ __launch_bounds__(kThreads, 1) void lmhead_logprob_kernel(LmheadArgs 
     }
   };
   auto issue = [&](int slice) {
-    prep_issue(slice);
+    prep_issue(slice, slice);
     if (!issue_tail) {
 #pragma unroll
       for (int j = 0; j < kDmaPerSlice; ++j) issue_one(j, std::false_type{});
@@ -291,13 +257,9 @@ __global__ __launch_bounds__(kThreads, 1) void lmhead_logprob_kernel(LmheadArgs 
   // ---- fragment reads ------------------------------------------------------
   // Fragments start at multiples of 16 rows, so a fragment row's swizzle is
   // that of (lane mod 16): one per-lane offset per K-step, plus immediates.
-  // Lane group g reads chunk 4 ks + sigma(g), sigma = (0, 2, 1, 3): a
-  // ds_read_b128 serves lanes i..i+7 together with lanes i+32..i+39, i.e.
-  // groups g and g + 2 of the same 8 rows, and those must read chunks c and
-  // c ^ 1, which the row swizzle places in disjoint bank sets (chunks c and
-  // c + 2 would collide two-way).  A and B use the same mapping, so the
-  // K positions still pair up.
-  const int kchunk = ((grp & 1) << 1) | (grp >> 1);
+  // Lane group g reads chunk 4 ks + frag_chunk(g) of the K-step (A and B
+  // alike, so the K positions pair up).
+  const int kchunk = frag_chunk(grp);
   const int frag_lane[kKSteps] = {(r16 * kChunks + ((0 + kchunk) ^ row_xor(r16))),
                                   (r16 * kChunks + ((4 + kchunk) ^ row_xor(r16)))};
   // the two W fragments (vocabulary blocks 2 pr, 2 pr + 1) of quarter pr of K-step ks
@@ -499,12 +461,11 @@ __global__ __launch_bounds__(kThreads, 1) void lmhead_logprob_kernel(LmheadArgs 
       } else {
         // As above, but the DMAs for slice it+kStages are spread between
         // this quarter's MFMAs so their issue overlaps matrix work.  They are
-        // unconditional: past the end of the work item they re-fetch the last
-        // slice into the stage just freed, which nothing reads.
+        // unconditional: past the end of the work item they fetch a copy of
+        // the last slice into the stage just freed, which nothing reads.
         wait_dma(kStages - 2);
         raw_barrier();
-        const int nxt = it + kStages < n_iter ? it + kStages : n_iter - 1;
-        prep_issue(nxt);
+        prep_issue(it + kStages, it + kStages < n_iter ? it + kStages : n_iter - 1);
         load_a(it + 1, 0, 0, fa[0]);
 #pragma unroll
         for (int bn = 0; bn < kTB; ++bn) load_b(it + 1, 0, bn, fb[0][bn]);

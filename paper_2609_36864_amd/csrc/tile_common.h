@@ -11,32 +11,31 @@ namespace hdl {
 namespace tile {
 
 typedef __bf16 bf16x8_t __attribute__((ext_vector_type(8)));
-typedef float f32x16_t __attribute__((ext_vector_type(16)));
 typedef float f32x4_t __attribute__((ext_vector_type(4)));
 
 constexpr int kWaves = 8;                           // two waves per SIMD
 constexpr int kThreads = 64 * kWaves;
-constexpr int kNB = 2;                              // 32-token MFMA blocks per wave
-constexpr int kWaveN = 32 * kNB;                    // tokens per wave
+constexpr int kVB = 8;                              // 16-row MFMA blocks per wave along M (128 rows)
+constexpr int kTB = 4;                              // 16-column MFMA blocks per wave along N
+constexpr int kWaveN = 16 * kTB;                    // N columns per wave
 constexpr int kChunks = 8;                          // 16-byte chunks per LDS row per stage (128-byte K-slices)
+constexpr int kKSteps = kChunks / 4;                // MFMA K-steps (4 chunks each) per K-slice
 constexpr int kStages = 2;                          // LDS ring depth (K-slices)
 constexpr int kSlots = kTileV * kChunks;            // uint4 slots per operand per stage
 constexpr int kBlockRows = 64 / kChunks;            // rows per 1 KB DMA block
 constexpr int kBlocksPerWave = kTileV / kBlockRows / kWaves;   // DMA blocks per operand per wave
 constexpr int kDmaPerSlice = 2 * kBlocksPerWave;    // DMA instructions per lane per slice
-constexpr int kSub = kChunks / 2;                   // MFMA sub-steps per slice
 constexpr float kLog2e = 1.4426950408889634f;
 constexpr float kNegInf = -__builtin_inff();
 
 static_assert(kTileV == kTileN, "square workgroup tile assumed");
+static_assert(2 * 16 * kVB == kTileV && 4 * kWaveN == kTileN, "8 waves as 2 (M) x 4 (N)");
 static_assert(kStages * 2 * kSlots * 16 <= 160 * 1024, "LDS ring exceeds 160 KB");
 static_assert(kDmaPerSlice * (kStages - 1) <= 63, "vmcnt range");
 
-// XOR pattern of a row: the rows of one 32-row fragment read must land in
-// distinct 16-byte bank groups whether the LDS serves 8 or 16 lanes of a
-// ds_read_b128 per cycle.  With 128-byte rows, (row & 7) ^ ((row >> 3) & 1)
-// does both: 8 consecutive rows get 8 distinct chunks, and rows r and r+8
-// (same bank half when two rows share a 256-byte bank line) differ too.
+// XOR pattern of a row of 128 bytes: 8 consecutive rows get 8 distinct
+// chunks, and rows r and r + 8 differ too, so a fragment read (16 rows; see
+// frag_chunk) touches every bank at most once per pass.
 __device__ __forceinline__ int row_xor(int row) { return (row & 7) ^ ((row >> 3) & 1); }
 
 // Slot of (row, logical 16-byte chunk) in a [rows][kChunks] LDS tile.
@@ -83,32 +82,40 @@ __device__ __forceinline__ void raw_barrier() {
   asm volatile("s_waitcnt lgkmcnt(0)\n\ts_barrier" ::: "memory");
 }
 
-// One MFMA step over a pair of 16-byte fragments (same K positions in A, B).
-template <bool BF16> struct Mma;
+// The MFMA shape of the tile kernels: v_mfma_f32_16x16x32_bf16 (fp32
+// inputs: four v_mfma_f32_16x16x4_f32 over one 16-byte fragment).  A
+// fragment is 16 rows (M or N indices) of one operand: lane l holds row
+// (l mod 16) and 16 bytes of consecutive K values, which lane group
+// g = l div 16 takes from 16-byte chunk 4 ks + frag_chunk(g) of K-step ks.
+// A and B fragments take the same K positions, so the contraction is exact
+// whatever order the hardware sums them in.  The 16 x 16 fp32 result block
+// sits in 4 registers per lane: column (l mod 16), rows 4 (l div 16) + i.
+template <bool BF16> struct Mma16;
 
-template <> struct Mma<true> {
-  static constexpr int kElemsPer16B = 8;
-  __device__ __forceinline__ static void run(const uint4& a, const uint4& b, f32x16_t& c) {
-    c = __builtin_amdgcn_mfma_f32_32x32x16_bf16(__builtin_bit_cast(bf16x8_t, a),
-                                                __builtin_bit_cast(bf16x8_t, b), c, 0, 0, 0);
+template <> struct Mma16<true> {
+  __device__ __forceinline__ static void run(const uint4& a, const uint4& b, f32x4_t& c) {
+    c = __builtin_amdgcn_mfma_f32_16x16x32_bf16(__builtin_bit_cast(bf16x8_t, a), __builtin_bit_cast(bf16x8_t, b), c,
+                                                0, 0, 0);
   }
 };
 
-template <> struct Mma<false> {
-  static constexpr int kElemsPer16B = 4;
-  // Four K=2 steps; lane group g supplies K offset 4g + j in step j, the same
-  // for both operands, so the four steps cover the fragment's 8 K values.
-  __device__ __forceinline__ static void run(const uint4& a, const uint4& b, f32x16_t& c) {
-    c = __builtin_amdgcn_mfma_f32_32x32x2f32(__uint_as_float(a.x), __uint_as_float(b.x), c, 0, 0, 0);
-    c = __builtin_amdgcn_mfma_f32_32x32x2f32(__uint_as_float(a.y), __uint_as_float(b.y), c, 0, 0, 0);
-    c = __builtin_amdgcn_mfma_f32_32x32x2f32(__uint_as_float(a.z), __uint_as_float(b.z), c, 0, 0, 0);
-    c = __builtin_amdgcn_mfma_f32_32x32x2f32(__uint_as_float(a.w), __uint_as_float(b.w), c, 0, 0, 0);
+template <> struct Mma16<false> {
+  // Four K = 4 steps; lane group g supplies K offset 4 g + j in step j, the
+  // same for both operands, so the four steps cover the fragment's 16 K values.
+  __device__ __forceinline__ static void run(const uint4& a, const uint4& b, f32x4_t& c) {
+    c = __builtin_amdgcn_mfma_f32_16x16x4f32(__uint_as_float(a.x), __uint_as_float(b.x), c, 0, 0, 0);
+    c = __builtin_amdgcn_mfma_f32_16x16x4f32(__uint_as_float(a.y), __uint_as_float(b.y), c, 0, 0, 0);
+    c = __builtin_amdgcn_mfma_f32_16x16x4f32(__uint_as_float(a.z), __uint_as_float(b.z), c, 0, 0, 0);
+    c = __builtin_amdgcn_mfma_f32_16x16x4f32(__uint_as_float(a.w), __uint_as_float(b.w), c, 0, 0, 0);
   }
 };
 
-// Row of the 32x32 accumulator block held in element i of lane l:
-// row = 8*(i/4) + 4*(l/32) + (i%4), column = l%32.
-__device__ __forceinline__ int acc_row(int i, int half) { return 8 * (i >> 2) + 4 * half + (i & 3); }
+// Which of a K-step's four 16-byte chunks lane group g reads: (0, 2, 1, 3).
+// A ds_read_b128 serves lanes i..i+7 together with lanes i+32..i+39, i.e.
+// lane groups g and g + 2 of the same 8 rows; they must read chunks c and
+// c ^ 1, which the row swizzle keeps in disjoint banks (chunks c and c + 2,
+// the identity mapping, collide two-way).
+__device__ __forceinline__ int frag_chunk(int grp) { return ((grp & 1) << 1) | (grp >> 1); }
 
 }  // namespace tile
 }  // namespace hdl

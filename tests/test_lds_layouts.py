@@ -1,30 +1,34 @@
-"""Invariants of the LDS layouts the backward GEMM reads with gfx950's
-transposing loads (ds_read_b64_tr_b16), checked on the CPU by enumeration.
+"""Invariants of the LDS layouts of the MFMA tile kernels, checked on the CPU
+by enumeration.
 
-The read's lane mapping, as measured on the GPU: within each group of 16
-lanes, lane i receives element i mod 4 of the 8-byte pieces addressed by
-lanes i/4, i/4 + 4, i/4 + 8 and i/4 + 12 of its group.
+Backward GEMM (lmhead_backward.hip).  Operands whose stored rows run along
+the contracted index K are read with gfx950's transposing load
+ds_read_b64_tr_b16, whose lane mapping, as measured on the GPU, is: within
+each group of 16 lanes, lane i receives element i mod 4 of the 8-byte pieces
+addressed by lanes i/4, i/4 + 4, i/4 + 8 and i/4 + 12 of its group.
 
-Layouts (16-byte slots; a K-slice holds 64 stored rows of 256 columns):
+Layouts (16-byte slots; a K-slice holds 64 stored K rows of 256 columns):
   K-row:        slot(row r, chunk c) = 32 r + (c ^ krow_xor(r))
-  chunk-major:  slot(row r, chunk c) = 64 c + (r ^ cm_xor(c))
-For each, a lane reading block columns m0 .. m0+31 at sub-step kk addresses
-row 16 kk + 8 half + 4 j + a/4 and column m0 + 16 g + 4 (a mod 4) (a = lane
-mod 16, g = (lane / 16) mod 2, half = lane / 32, j = which 4 of its 8 K
-values).  Checked: the result is the MFMA operand (column m0 + lane mod 32,
-K values 8 half .. 8 half + 7 of the sub-step, in order), and the 16- and
-32-lane subsets a transposing read serves together land in distinct bank
-ranges whether the LDS serves 128 or 256 bytes per clock.
+  chunk-major:  slot(row r, chunk c) = 64 c + (r ^ cm_xor(c, r))
+For the 16-column fragment m0 .. m0+15 at K-step ks, lane a of lane group g
+addresses K row 32 ks + 8 sigma(g) + 4 j + a/4 and column m0 + 4 (a mod 4)
+(read j = 0, 1; sigma = (0, 2, 1, 3), the K chunk each lane group takes in
+every tile kernel).  Checked: the result is the MFMA operand (column
+m0 + lane mod 16, K values 8 sigma(g) .. 8 sigma(g) + 7 of the K-step, in
+order), and the lanes a read serves together touch distinct banks whether
+the LDS serves 16 lanes (128 bytes) or 32 lanes (256 bytes) per clock, and
+for either pairing of 16-lane groups.
 """
+
+SIGMA = (0, 2, 1, 3)
 
 
 def krow_xor(r):
-    j0, j1 = r & 1, (r >> 1) & 1
-    return 2 * j1 + 4 * j0 + 8 * (j0 ^ j1)
+    return 2 * ((r & 3) | ((((r >> 3) ^ (r >> 4)) & 1) << 2))
 
 
-def cm_xor(c):
-    return 4 * (c & 3)
+def cm_xor(c, r):
+    return (4 * (c & 1)) ^ (8 * ((r >> 4) & 1))
 
 
 def slot_krow(r, c):
@@ -32,19 +36,19 @@ def slot_krow(r, c):
 
 
 def slot_cm(r, c):
-    return 64 * c + (r ^ cm_xor(c))
+    return 64 * c + (r ^ cm_xor(c, r))
 
 
-def lane_address(slot_fn, lane, kk, j, m0):
-    a, g, half = lane & 15, (lane >> 4) & 1, lane >> 5
-    r = 16 * kk + 8 * half + 4 * j + a // 4
-    m = m0 + 16 * g + 4 * (a % 4)
+def lane_address(slot_fn, lane, ks, j, m0):
+    a, g = lane & 15, lane >> 4
+    r = 32 * ks + 8 * SIGMA[g] + 4 * j + a // 4
+    m = m0 + 4 * (a % 4)
     return slot_fn(r, m // 8) * 16 + (m % 8) * 2, (r, m)
 
 
-def transposed_read(slot_fn, kk, j, m0):
+def transposed_read(slot_fn, ks, j, m0):
     """Emulate one ds_read_b64_tr_b16: per lane, the 4 (row, column) elements received."""
-    addr = [lane_address(slot_fn, l, kk, j, m0) for l in range(64)]
+    addr = [lane_address(slot_fn, l, ks, j, m0) for l in range(64)]
     out = []
     for l in range(64):
         g0, i = (l // 16) * 16, l % 16
@@ -60,35 +64,66 @@ def test_xor_patterns_are_bijections():
     for r in range(64):
         assert sorted(c ^ krow_xor(r) for c in range(32)) == list(range(32))
     for c in range(32):
-        assert sorted(r ^ cm_xor(c) for r in range(64)) == list(range(64))
+        assert sorted(r ^ cm_xor(c, r) for r in range(64)) == list(range(64))
+        # the DMA side inverts the chunk-major pattern by applying it again
+        assert all((r ^ cm_xor(c, r)) ^ cm_xor(c, r ^ cm_xor(c, r)) == r for r in range(64))
 
 
 def test_transposed_reads_deliver_mfma_fragments():
     for slot_fn in (slot_krow, slot_cm):
-        for kk in range(4):
-            for m0 in range(0, 256, 32):
-                got = [transposed_read(slot_fn, kk, j, m0) for j in range(2)]
+        for ks in range(2):
+            for m0 in range(0, 256, 16):
+                got = [transposed_read(slot_fn, ks, j, m0) for j in range(2)]
                 for l in range(64):
                     frag = got[0][l] + got[1][l]
-                    want = [(16 * kk + 8 * (l >> 5) + t, m0 + (l & 31)) for t in range(8)]
-                    assert frag == want, (slot_fn.__name__, kk, m0, l)
+                    want = [(32 * ks + 8 * SIGMA[l >> 4] + t, m0 + (l & 15)) for t in range(8)]
+                    assert frag == want, (slot_fn.__name__, ks, m0, l)
+
+
+def _collisions(addrs, lanes, nbytes, width):
+    banks = {}
+    for l in lanes:
+        for b in range(addrs[l], addrs[l] + nbytes, 4):
+            banks.setdefault((b % width) // 4, set()).add(b)
+    return max(len(v) for v in banks.values())
 
 
 def test_transposed_reads_are_bank_conflict_free():
-    # 64 banks x 4 bytes; a request set is conflict-free when no two lanes
-    # touch different addresses in the same bank within one served group
+    groups = [(128, [list(range(i, i + 16)) for i in range(0, 64, 16)]),      # 16 lanes per clock
+              (256, [list(range(0, 32)), list(range(32, 64))]),               # 32 consecutive lanes
+              (256, [list(range(0, 16)) + list(range(32, 48)),                # or groups g and g + 2
+                     list(range(16, 32)) + list(range(48, 64))])]
     for slot_fn in (slot_krow, slot_cm):
-        for kk in range(4):
-            for m0 in range(0, 256, 32):
+        for ks in range(2):
+            for m0 in range(0, 256, 16):
                 for j in range(2):
-                    addrs = [lane_address(slot_fn, l, kk, j, m0)[0] for l in range(64)]
-                    for width, group in ((128, 16), (256, 32)):   # bytes per clock, lanes served together
-                        for g0 in range(0, 64, group):
-                            seen = {}
-                            for a in addrs[g0:g0 + group]:
-                                for b in range(a, a + 8, 4):
-                                    bank = (b % width) // 4
-                                    assert seen.setdefault(bank, b) == b, (slot_fn.__name__, width, kk, m0, j)
+                    addrs = [lane_address(slot_fn, l, ks, j, m0)[0] for l in range(64)]
+                    for width, sets in groups:
+                        for lanes in sets:
+                            assert _collisions(addrs, lanes, 8, width) == 1, (slot_fn.__name__, width, ks, m0, j)
+
+
+def test_chunk_major_plain_reads_pair_like_the_measured_layout():
+    # The plain (ds_read_b128) reads of the GEMM's chunk-major operands:
+    # slot c * 256 + i, lane l reads row m0 + l mod 16 of chunk
+    # 4 ks + sigma(l div 16).  Lanes i..i+7 and i+32..i+39 then read the
+    # same 8 rows of chunks 2 m and 2 m + 1, the pairing the 32-row
+    # fragments of this layout used (lane l: row l mod 32, chunk
+    # 2 kk + l div 32), for which the counters showed no bank conflict; and
+    # every 16 consecutive lanes read 256 contiguous bytes.
+    for m0 in range(0, 256, 16):
+        for ks in range(2):
+            slot = [(4 * ks + SIGMA[l >> 4]) * 256 + m0 + (l & 15) for l in range(64)]
+            for i in range(0, 32, 8):
+                lo = [slot[l] for l in range(i, i + 8)]
+                hi = [slot[l] for l in range(i + 32, i + 40)]
+                assert [h - x for x, h in zip(lo, hi)] == [256] * 8
+                assert (lo[0] // 256) % 2 == 0
+            for g in range(4):
+                s16 = slot[16 * g:16 * g + 16]
+                assert s16 == list(range(s16[0], s16[0] + 16))
+            # every lane group's 8 K values: chunk 4 ks + sigma(g)
+            assert sorted({s // 256 for s in slot}) == [4 * ks + c for c in range(4)]
 
 
 # ---- the fused lm-head kernel's 16 x 16 x 32 fragment reads ---------------
