@@ -25,6 +25,25 @@ def as_f64(t: torch.Tensor) -> np.ndarray:
     return t.double().numpy()
 
 
+# Gradient tolerance (the backward pass rounds the logit gradient G once to
+# bf16).  bf16 has 8 significant bits, so round-to-nearest moves an element
+# by at most 2^-8 of itself, and an output element sum_v G W (or sum_n G h)
+# by at most 2^-8 times the magnitude sum sum_v |G| |W| -- a worst case that
+# is nearly reached where one term dominates the sum, as the sampled token's
+# column g (1 - p_y) does in dL/dh.  The fp32 accumulation over K terms
+# (error growing like sqrt(K) 2^-24, below 2^-15 of the magnitude sum for
+# K <= 2^18) and the fp32 evaluation of p (a few ulps) come on top: the tests
+# allow 2^-12 of the magnitude sum for them, and 1e-6 of the largest
+# magnitude sum for outputs whose own sum is near zero.
+GRAD_ROUND = 2.0 ** -8
+GRAD_EXTRA = 2.0 ** -12
+
+
+def grad_tol(mag: np.ndarray, extra=0.0) -> np.ndarray:
+    """Allowed |GPU - oracle| of a gradient element with magnitude sum mag."""
+    return (GRAD_ROUND + GRAD_EXTRA) * mag + extra + 1e-6 * mag.max()
+
+
 def flat_inputs(w):
     """Row-major inputs of one call covering both contexts."""
     return w.rows_hidden(), w.W, w.rows_tokens(), w.rows_mask()

@@ -2,12 +2,12 @@
 (gradients of sum_n g_n log p_n(y_n), the token-level policy loss of Sec. 3.3)
 against the float64 oracle, through the C ABI.
 
-Tolerance (derived from the arithmetic): the library rounds the logit
-gradient G = g (1[v == y] - p) to bf16 (relative error <= 2^-9 per element)
-and accumulates in fp32, so each element of dH = G W and dW = G^T H may move
-by at most 2^-9 sum |G| |W| (resp. sum |G| |h|) plus fp32 accumulation
-error; the tests allow 2^-8 times the oracle's magnitude sums plus 1e-6 of
-the largest magnitude.
+Tolerance (derived from the arithmetic, tests/gpu_helpers.grad_tol): the
+library rounds the logit gradient G = g (1[v == y] - p) to bf16 (relative
+error <= 2^-8 per element: 8 significant bits) and accumulates in fp32, so
+each element of dH = G W and dW = G^T H may move by at most 2^-8 sum |G| |W|
+(resp. sum |G| |h|) plus the fp32 accumulation error; the tests allow
+(2^-8 + 2^-12) times the oracle's magnitude sums plus 1e-6 of the largest.
 """
 import numpy as np
 import pytest
@@ -15,7 +15,7 @@ import torch
 
 import workloads
 from oracle import hdl_oracle as O
-from tests.gpu_helpers import as_f64, require_gpu
+from tests.gpu_helpers import as_f64, grad_tol, require_gpu
 
 pytestmark = pytest.mark.gpu
 
@@ -45,7 +45,7 @@ def _gpu(hdl, H, W, y, m, up, **kw):
 
 
 def _check(got, want, mag, what):
-    tol = 2.0 ** -8 * mag + 1e-6 * mag.max()
+    tol = grad_tol(mag)
     bad = np.abs(got - want) > tol
     assert not bad.any(), (f"{what}: {bad.sum()} elements out of bound, worst excess "
                            f"{(np.abs(got - want) - tol).max():.3g}")
@@ -127,12 +127,15 @@ def test_backward_out_of_range_token_and_argument_errors(hdl):
                                     torch.zeros(64, device="cuda"), up.cuda())
 
 
-def test_backward_full_size_sampled_rows(hdl):
+def test_backward_full_size_every_row_tile(hdl):
     # the benchmark's configuration (8 roots x 4096 tokens of the original
-    # context, d = 2048, V = 151,936): dH on sampled rows against the oracle,
-    # and for dW a property that holds at any size: the vocabulary rows of
-    # dW sum to sum_n (sum_v G_nv) h_n = 0, up to the bf16 rounding of G,
-    # |sum_v dG_nv| <= 2^-9 sum_v |G_nv| <= 2^-8 |g_n|
+    # context, d = 2048, V = 151,936, one chunk of 32,512 trained rows):
+    # dH of one seeded row from every 256-row tile of the trained rows (the
+    # GEMM's M tiles, in the library's compaction order) and of the last
+    # trained row, against the oracle; for dW a property that holds at any
+    # size: the vocabulary rows of dW sum to sum_n (sum_v G_nv) h_n = 0, up
+    # to the bf16 rounding of G, |sum_v dG_nv| <= 2^-8 sum_v |G_nv| <= 2^-7 |g_n|
+    # (sum_v |G_nv| = 2 |g_n| (1 - p_n(y_n)))
     w = workloads.make_workload("c2")
     c = w.cfg
     n0 = c.R * c.T
@@ -141,12 +144,18 @@ def test_backward_full_size_sampled_rows(hdl):
     m = w.rows_mask()[:n0]
     up = torch.from_numpy(np.random.default_rng(11).normal(size=n0).astype(np.float32))
     dh, dw = _gpu(hdl, H, w.W, y, m, up)
-    rows = np.array([40, 5000, 17777, n0 - 1])
-    assert np.all(m.numpy()[rows] == 1)
+    trained = np.nonzero(m.numpy())[0]
+    rng = np.random.default_rng(c.seed + 7)
+    pick = [int(rng.integers(t0, min(t0 + 256, len(trained)))) for t0 in range(0, len(trained), 256)]
+    rows = trained[np.array(sorted(set(pick + [len(trained) - 1])))]
     want_dh, _, mag_dh, _ = O.token_logprobs_backward(as_f64(H[torch.as_tensor(rows)]), as_f64(w.W),
                                                       y.numpy()[rows], up.double().numpy()[rows])
-    _check(dh[rows], want_dh, mag_dh, "dH (sampled rows)")
+    err = np.abs(dh[rows] - want_dh)
+    print(f"\nc2 backward: dH of {len(rows)} rows (one per 256-row tile): max |error| {err.max():.3g}, "
+          f"max |error| / bound {(err / grad_tol(mag_dh)).max():.3g}")
+    _check(dh[rows], want_dh, mag_dh, "dH (one row per tile)")
     keep = m.numpy() != 0
-    bound = 2.0 ** -8 * (np.abs(up.double().numpy()[keep])[:, None] * np.abs(as_f64(H)[keep])).sum(0)
+    assert np.all(dh[~keep] == 0)
+    bound = 2.0 ** -7 * (np.abs(up.double().numpy()[keep])[:, None] * np.abs(as_f64(H)[keep])).sum(0)
     colsum = dw.sum(axis=0)
     assert np.all(np.abs(colsum) <= bound + 1e-6 * np.abs(dw).max())
