@@ -201,7 +201,8 @@ def main() -> int:
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--cpu-budget", type=float, default=15.0)
     ap.add_argument("--no-mfma-ceiling", action="store_true",
-                    help="skip measuring this GPU's MFMA ceilings (const/random operands) and the "
+                    help="skip measuring this GPU's ceilings of the kernel's main loop (MFMAs on "
+                         "const/random operands, with LDS reads, with the per-slice DMA) and the "
                          "library GEMM reference")
     ap.add_argument("--copy-probe-mb", type=int, default=0,
                     help="after timing, copy this many MiB device-to-device once (a known-size "
@@ -249,7 +250,8 @@ def main() -> int:
     logp = torch.empty(n_rows, dtype=torch.float32, device=dev)
     ent = torch.empty(n_rows, dtype=torch.float32, device=dev)
     torch.cuda.synchronize()
-    log(f"inputs resident on {torch.cuda.get_device_name(0)}: {n_rows} rows, {n_scored} scored")
+    props = torch.cuda.get_device_properties(0)
+    log(f"inputs resident on {props.name or getattr(props, 'gcnArchName', 'cuda:0')}: {n_rows} rows, {n_scored} scored")
 
     def step():
         if ent_sel:
@@ -350,6 +352,8 @@ def main() -> int:
         ceil = mfma_ceiling()
         if ceil is not None:
             ceil["frac_of_random_operand_ceiling"] = achieved / ceil["random_operands_tflops"]
+            if ceil.get("slice_loop_dma_hbm_tflops"):
+                ceil["frac_of_slice_loop_ceiling"] = achieved / ceil["slice_loop_dma_hbm_tflops"]
             result["roofline"]["measured_ceiling"] = ceil
             log(f"MFMA ceilings: {ceil}")
         lib = library_gemm_tflops(hidden[mask.bool()], W)

@@ -1,102 +1,194 @@
-// Measured bf16 MFMA ceilings of the GPU this runs on (a measurement tool for
-// the fused lm-head kernel's roofline; not part of libhdl.so).
+// Measured ceilings of the fused lm-head kernel's main loop on the GPU this
+// runs on (a measurement tool for the kernel's roofline; not part of
+// libhdl.so).
 //
-// Three loops, each on every CU with 8 waves (2 per SIMD) and
-// v_mfma_f32_32x32x16_bf16 into 4x2 independent 32x32 accumulator blocks per
-// wave -- the same instruction, block shape and occupancy as the fused kernel:
-//   const  : operands with few set bits (bf16 1.0) -- the instruction-rate ceiling;
-//   random : pseudo-random bf16 operands, as real weights and hidden states --
-//            MFMA power rises with operand bit activity, so this ceiling is lower;
-//   mixed  : random operands re-read from LDS every sub-step (6 ds_read_b128
-//            fragments per 8 MFMAs, swizzled as in the fused kernel).
-// Prints one JSON object with TFLOP/s for each.  Every LDS index is masked into
-// range and every loop is bounded.
+// Every loop runs on every CU with the kernel's shape: 8 waves (2 per SIMD),
+// each 128 x 64 of a 256 x 256 tile as 8 x 4 blocks of
+// v_mfma_f32_16x16x32_bf16, a K-slice being 2 K-steps x 4 quarters of 8
+// MFMAs.  Step by step towards the kernel:
+//   const      : operands held in registers, few set bits (bf16 1.0) -- the
+//                instruction-rate ceiling;
+//   random     : random bf16 operands in registers -- MFMA power rises with
+//                operand bit activity, so the clock and this ceiling are lower;
+//   lds        : random operands read from a 2-stage LDS ring every quarter
+//                with the kernel's swizzle, fragment mapping and read-ahead,
+//                one workgroup barrier per slice;
+//   dma_l2     : as lds, plus the kernel's per-slice global -> LDS DMA of the
+//                stage just freed (8 x 1 KB per wave, 128-byte runs of rows
+//                4 KB apart) from a 4 MB source that stays in L2;
+//   dma_hbm    : the same from a 1 GiB source (L2 misses to HBM).
+// Prints one JSON object with TFLOP/s for each.  Every LDS index is in range
+// by construction, every DMA source address lies inside its buffer, and every
+// loop is bounded.
 #include <hip/hip_runtime.h>
 
+#include <cstdint>
 #include <cstdio>
 
 namespace {
 
 typedef __bf16 bf16x8_t __attribute__((ext_vector_type(8)));
-typedef float f32x16_t __attribute__((ext_vector_type(16)));
+typedef float f32x4_t __attribute__((ext_vector_type(4)));
 
-__device__ __forceinline__ int slot(int row, int chunk) {
-  return row * 8 + (chunk ^ ((row & 7) ^ ((row >> 3) & 1)));
-}
+constexpr int kSlots = 2048;                 // 256 rows x 8 sixteen-byte chunks per operand stage
+constexpr uint64_t kRegion = 256ull * 4096;  // DMA source of one slice: 256 rows 4 KB apart
+
+__device__ __forceinline__ int row_xor(int r) { return (r & 7) ^ ((r >> 3) & 1); }
 
 __device__ __forceinline__ uint32_t mix32(uint32_t x) {
   x ^= x >> 15; x *= 0x2c1b3c6du; x ^= x >> 12; x *= 0x297a2d39u; x ^= x >> 15;
   return x;
 }
 
-// MODE 0: constant operands, no LDS reads; 1: random operands, no LDS reads;
-// 2: random operands re-read from LDS each sub-step.
+// two bf16 values with exponents near 1 and random sign and mantissa bits
+__device__ __forceinline__ uint32_t rand_pair(uint32_t x) {
+  return (0x3e00u | (x & 0x80ffu)) | ((0x3e00u | ((x >> 16) & 0x80ffu)) << 16);
+}
+
+__device__ __forceinline__ void dma16(uint64_t sbase, uint32_t voff, uint32_t lds_base) {
+  uint32_t saved;
+  asm volatile(
+      "s_mov_b32 %0, m0\n\t"
+      "s_mov_b32 m0, %1\n\t"
+      "s_nop 0\n\t"
+      "global_load_lds_dwordx4 %2, %3\n\t"
+      "s_mov_b32 m0, %0"
+      : "=&s"(saved)
+      : "s"(lds_base), "v"(voff), "s"(sbase)
+      : "memory");
+}
+
+__global__ void fill_random(uint32_t* p, uint64_t n) {
+  for (uint64_t i = blockIdx.x * 256ull + threadIdx.x; i < n; i += 256ull * gridDim.x)
+    p[i] = rand_pair(mix32(static_cast<uint32_t>(i) * 2654435761u + 0x9e3779b9u));
+}
+
+// MODE 0 const, 1 random (registers only); 2 lds; 3 lds + DMA (the source
+// size decides L2 or HBM).
 template <int MODE>
-__global__ __launch_bounds__(512) void ceiling_kernel(float* out, int iters) {
-  __shared__ uint4 lds[2][2048];   // 64 KB: [A/B][256 rows x 8 chunks]
-  for (int i = threadIdx.x; i < 4096; i += 512) {
+__global__ __launch_bounds__(512, 1) void ceiling_kernel(const char* __restrict__ src, uint64_t n_regions,
+                                                          float* out, int slices) {
+  __shared__ uint4 lds[2][2][kSlots];   // [stage][A/B], 128 KB like the kernel's ring
+  const int tid = threadIdx.x, lane = tid & 63;
+  const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);
+  const int wm = wave & 1, wn = wave >> 1, r16 = lane & 15, grp = lane >> 4;
+  for (int i = tid; i < 2 * 2 * kSlots; i += 512) {
     uint32_t h[4];
-    for (int q = 0; q < 4; ++q) {
-      const uint32_t x = mix32(static_cast<uint32_t>(i * 4 + q) * 2654435761u + 0x9e3779b9u * (blockIdx.x + 1));
-      // two bf16 values with exponents near 1 and random sign/mantissa bits
-      h[q] = MODE == 0 ? 0x3f803f80u : ((0x3e00u | (x & 0x80ffu)) | ((0x3e00u | ((x >> 16) & 0x80ffu)) << 16));
-    }
-    (&lds[0][0])[i] = make_uint4(h[0], h[1], h[2], h[3]);
+    for (int q = 0; q < 4; ++q)
+      h[q] = MODE == 0 ? 0x3f803f80u : rand_pair(mix32(static_cast<uint32_t>(i * 4 + q) * 2654435761u +
+                                                       0x9e3779b9u * (blockIdx.x + 1)));
+    (&lds[0][0][0])[i] = make_uint4(h[0], h[1], h[2], h[3]);
   }
   __syncthreads();
-  const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6, wm = wave & 1, wn = wave >> 1;
-  const int col = lane & 31, half = lane >> 5;
-  f32x16_t acc[4][2];
-  for (int a = 0; a < 4; ++a)
-    for (int b = 0; b < 2; ++b)
-      for (int q = 0; q < 16; ++q) acc[a][b][q] = 0.f;
-  uint4 fa[2][4], fb[2][2];
-  for (int bm = 0; bm < 4; ++bm) fa[0][bm] = lds[0][slot(wm * 128 + bm * 32 + col, half)];
-  for (int bn = 0; bn < 2; ++bn) fb[0][bn] = lds[1][slot(wn * 64 + bn * 32 + col, half)];
-  for (int it = 0; it < iters; ++it) {
+  f32x4_t acc[8][4];
 #pragma unroll
-    for (int kk = 0; kk < 4; ++kk) {
-      const int cur = kk & 1, nk = (kk + 1) & 3;
-      if (MODE == 2) {
+  for (int a = 0; a < 8; ++a)
 #pragma unroll
-        for (int bm = 0; bm < 4; ++bm) fa[cur ^ 1][bm] = lds[0][slot(wm * 128 + bm * 32 + col, nk * 2 + half)];
+    for (int b = 0; b < 4; ++b) acc[a][b] = f32x4_t{0.f, 0.f, 0.f, 0.f};
+  const int kchunk = ((grp & 1) << 1) | (grp >> 1);
+  const int frag[2] = {r16 * 8 + ((0 + kchunk) ^ row_xor(r16)), r16 * 8 + ((4 + kchunk) ^ row_xor(r16))};
+  auto load_a = [&](int st, int ks, int pr, uint4 (&d)[2]) {
 #pragma unroll
-        for (int bn = 0; bn < 2; ++bn) fb[cur ^ 1][bn] = lds[1][slot(wn * 64 + bn * 32 + col, nk * 2 + half)];
-        __builtin_amdgcn_sched_barrier(0);
+    for (int j = 0; j < 2; ++j) d[j] = lds[st][0][frag[ks] + (wm * 128 + (2 * pr + j) * 16) * 8];
+  };
+  auto load_b = [&](int st, int ks, int bn, uint4& d) { d = lds[st][1][frag[ks] + (wn * 64 + bn * 16) * 8]; };
+  auto mfma = [&](const uint4& a, const uint4& b, f32x4_t& c) {
+    c = __builtin_amdgcn_mfma_f32_16x16x32_bf16(__builtin_bit_cast(bf16x8_t, a), __builtin_bit_cast(bf16x8_t, b), c,
+                                                0, 0, 0);
+  };
+  auto quarter = [&](const uint4 (&a)[2], const uint4 (&b)[4], int pr) {
+#pragma unroll
+    for (int j = 0; j < 2; ++j)
+#pragma unroll
+      for (int bn = 0; bn < 4; ++bn) mfma(a[j], b[bn], acc[2 * pr + j][bn]);
+  };
+  const uint32_t lds_base = static_cast<uint32_t>(
+      reinterpret_cast<size_t>((__attribute__((address_space(3))) uint4*)(&lds[0][0][0])));
+  // DMA block i of this wave: rows 8 (4 w + i) .. + 7 of the region, lane l
+  // at row + l / 8, 16-byte chunk l % 8 (the kernel's pattern); < kRegion
+  uint32_t off[4];
+#pragma unroll
+  for (int i = 0; i < 4; ++i) off[i] = static_cast<uint32_t>(((wave * 4 + i) * 8 + lane / 8) * 4096 + (lane % 8) * 16);
+
+  uint4 fa[2][2], fb[2][4];
+  load_a(0, 0, 0, fa[0]);
+#pragma unroll
+  for (int bn = 0; bn < 4; ++bn) load_b(0, 0, bn, fb[0][bn]);
+  for (int it = 0; it < slices; ++it) {
+    const int st = MODE >= 2 ? (it & 1) : 0;
+#pragma unroll
+    for (int pr = 0; pr < 4; ++pr) {
+      if (MODE >= 2) {
+        if (pr < 3) load_a(st, 0, pr + 1, fa[(pr + 1) & 1]);
+        else load_a(st, 1, 0, fa[0]);
+        load_b(st, 1, pr, fb[1][pr]);
       } else {
-        for (int bm = 0; bm < 4; ++bm) fa[cur ^ 1][bm] = fa[cur][bm];
-        for (int bn = 0; bn < 2; ++bn) fb[cur ^ 1][bn] = fb[cur][bn];
+        fa[(pr + 1) & 1][0] = fa[pr & 1][0]; fa[(pr + 1) & 1][1] = fa[pr & 1][1];
+        fb[1][pr] = fb[0][pr];
       }
+      __builtin_amdgcn_sched_barrier(0);
+      quarter(fa[pr & 1], fb[0], pr);
+    }
 #pragma unroll
-      for (int j = 0; j < 8; ++j)
-        acc[j >> 1][j & 1] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(
-            __builtin_bit_cast(bf16x8_t, fa[cur][j >> 1]), __builtin_bit_cast(bf16x8_t, fb[cur][j & 1]),
-            acc[j >> 1][j & 1], 0, 0, 0);
+    for (int pr = 0; pr < 3; ++pr) {
+      if (MODE >= 2) load_a(st, 1, pr + 1, fa[(pr + 1) & 1]);
+      else { fa[(pr + 1) & 1][0] = fa[pr & 1][0]; fa[(pr + 1) & 1][1] = fa[pr & 1][1]; }
+      __builtin_amdgcn_sched_barrier(0);
+      quarter(fa[pr & 1], fb[1], pr);
+    }
+    // slice boundary: wait for this wave's DMA, workgroup barrier, then the
+    // DMA of the slice after next into the stage just read
+    if (MODE >= 3) asm volatile("s_waitcnt vmcnt(0)" ::: "memory");
+    if (MODE >= 2) asm volatile("s_waitcnt lgkmcnt(0)\n\ts_barrier" ::: "memory");
+    if (MODE >= 2) {
+      load_a(st ^ 1, 0, 0, fa[0]);
+#pragma unroll
+      for (int bn = 0; bn < 4; ++bn) load_b(st ^ 1, 0, bn, fb[0][bn]);
+    } else {
+      fa[0][0] = fa[1][0]; fa[0][1] = fa[1][1];
+#pragma unroll
+      for (int bn = 0; bn < 4; ++bn) fb[0][bn] = fb[1][bn];
+    }
+    __builtin_amdgcn_sched_barrier(0);
+    const uint64_t sbase = reinterpret_cast<uint64_t>(src) +
+                           ((static_cast<uint64_t>(blockIdx.x) + it) % n_regions) * kRegion;
+#pragma unroll
+    for (int j = 0; j < 8; ++j) {
+      mfma(fa[1][j / 4], fb[1][j % 4], acc[6 + j / 4][j % 4]);
+      if (MODE >= 3) {
+        const int op = j / 4, blk = j % 4;
+        dma16(sbase, off[blk],
+              __builtin_amdgcn_readfirstlane(lds_base + static_cast<uint32_t>(((st * 2 + op) * kSlots +
+                                                                               (wave * 4 + blk) * 64) * 16)));
+      }
     }
   }
+  asm volatile("s_waitcnt vmcnt(0)" ::: "memory");
   float s = 0.f;
-  for (int a = 0; a < 4; ++a)
-    for (int b = 0; b < 2; ++b)
-      for (int q = 0; q < 16; ++q) s += acc[a][b][q];
+#pragma unroll
+  for (int a = 0; a < 8; ++a)
+#pragma unroll
+    for (int b = 0; b < 4; ++b) s += acc[a][b][0] + acc[a][b][1] + acc[a][b][2] + acc[a][b][3];
   out[blockIdx.x * 512 + threadIdx.x] = s;
 }
 
 template <int MODE>
-double measure(float* out, int blocks, int iters) {
+double measure(const char* src, uint64_t n_regions, float* out, int blocks, int slices) {
   hipEvent_t e0, e1;
   if (hipEventCreate(&e0) != hipSuccess || hipEventCreate(&e1) != hipSuccess) return -1.0;
-  float ms = 0.f;
-  for (int rep = 0; rep < 2; ++rep) {   // the first launch warms clocks and caches
+  float ms = 0.f, best = 1e30f;
+  for (int rep = 0; rep < 3; ++rep) {   // the first launch warms clocks and caches
     if (hipEventRecord(e0) != hipSuccess) return -1.0;
-    hipLaunchKernelGGL(ceiling_kernel<MODE>, dim3(blocks), dim3(512), 0, 0, out, iters);
+    hipLaunchKernelGGL(ceiling_kernel<MODE>, dim3(blocks), dim3(512), 0, 0, src, n_regions, out, slices);
     if (hipGetLastError() != hipSuccess || hipEventRecord(e1) != hipSuccess) return -1.0;
     if (hipEventSynchronize(e1) != hipSuccess) return -1.0;
     if (hipEventElapsedTime(&ms, e0, e1) != hipSuccess) return -1.0;
+    if (rep > 0 && ms < best) best = ms;
   }
   (void)hipEventDestroy(e0);
   (void)hipEventDestroy(e1);
-  const double flops = static_cast<double>(blocks) * 8 * iters * 4 * 8 * (2.0 * 32 * 32 * 16);
-  return flops / (ms * 1e-3) / 1e12;
+  const double flops = static_cast<double>(blocks) * slices * (2.0 * 256 * 256 * 64);
+  return flops / (best * 1e-3) / 1e12;
 }
 
 }  // namespace
@@ -107,21 +199,30 @@ int main() {
     std::fprintf(stderr, "no GPU\n");
     return 1;
   }
-  const int blocks = prop.multiProcessorCount * 2;
-  const int iters = 3000;
+  const int blocks = prop.multiProcessorCount * 4;
+  const int slices = 1500;
+  const uint64_t big = 1ull << 30, small = 4ull << 20;
+  char* src = nullptr;
   float* out = nullptr;
+  if (hipMalloc(&src, big) != hipSuccess) return 1;
   if (hipMalloc(&out, static_cast<size_t>(blocks) * 512 * sizeof(float)) != hipSuccess) return 1;
-  const double c = measure<0>(out, blocks, iters);
-  const double r = measure<1>(out, blocks, iters);
-  const double m = measure<2>(out, blocks, iters);
+  hipLaunchKernelGGL(fill_random, dim3(4096), dim3(256), 0, 0, reinterpret_cast<uint32_t*>(src), big / 4);
+  if (hipDeviceSynchronize() != hipSuccess) return 1;
+  const double c = measure<0>(src, 1, out, blocks, slices);
+  const double r = measure<1>(src, 1, out, blocks, slices);
+  const double l = measure<2>(src, 1, out, blocks, slices);
+  const double d2 = measure<3>(src, small / kRegion, out, blocks, slices);
+  const double dh = measure<3>(src, big / kRegion, out, blocks, slices);
   (void)hipFree(out);
-  if (c < 0 || r < 0 || m < 0) {
+  (void)hipFree(src);
+  if (c < 0 || r < 0 || l < 0 || d2 < 0 || dh < 0) {
     std::fprintf(stderr, "kernel failed\n");
     return 1;
   }
-  std::printf("{\"instruction\": \"v_mfma_f32_32x32x16_bf16\", \"cus\": %d, "
+  std::printf("{\"instruction\": \"v_mfma_f32_16x16x32_bf16\", \"cus\": %d, "
               "\"const_operands_tflops\": %.1f, \"random_operands_tflops\": %.1f, "
-              "\"random_operands_with_lds_reads_tflops\": %.1f}\n",
-              prop.multiProcessorCount, c, r, m);
+              "\"slice_loop_lds_tflops\": %.1f, \"slice_loop_dma_l2_tflops\": %.1f, "
+              "\"slice_loop_dma_hbm_tflops\": %.1f}\n",
+              prop.multiProcessorCount, c, r, l, d2, dh);
   return 0;
 }
