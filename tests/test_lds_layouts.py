@@ -134,7 +134,7 @@ def test_chunk_major_plain_reads_pair_like_the_measured_layout():
 # i+32..i+39 (i = 0, 8, 16, 24) from 64 four-byte banks; under that model
 # sigma = (0, 2, 1, 3) is conflict-free and the identity is not (it collides
 # two-way in every pass, as the 4-per-read SQ_LDS_BANK_CONFLICT count of the
-# identity layout said).  The same model leaves the round-1 32 x 32 reads
+# identity layout said).  The same model leaves the earlier 32 x 32 reads
 # (lane l: row l mod 32, chunk 2 kk + l div 32) conflict-free, as measured.
 
 
