@@ -2,7 +2,9 @@
 log p, lse and the next-token entropy for every scored row (Eq. 1; the
 Entropy baseline of Sec. 4.1), and for bf16 inputs dL/dh and dL/dW of the
 token-level loss (Sec. 3.3).  The shapes are drawn once from a fixed seed so
-the cases are the same on every run; together they hit ragged row tiles,
+the cases are the same on every run (48 of them: 16 small, 32 wider, with
+up to 3,000 rows, d up to 1,024 and vocabularies up to 40,000); together
+they hit ragged row tiles,
 ragged vocabulary tiles (down to V = 1), K tails (d not a multiple of 64)
 and sparse or dense masks.
 
@@ -31,6 +33,15 @@ def _cases():
         V = int(rng.choice([1, 2, int(rng.integers(3, 600)), int(rng.integers(600, 6000))],
                            p=[0.1, 0.1, 0.3, 0.5]))
         density = float(rng.choice([1.0, 0.7, 0.05]))
+        out.append((i, bf16, n, d, V, density))
+    # wider shapes: up to 3,000 rows, d up to 1,024, vocabularies up to 40,000
+    rng = np.random.default_rng(20261203)
+    for i in range(16, 48):
+        bf16 = i % 5 != 4
+        n = int(rng.integers(1, 3000))
+        d = 8 * int(rng.integers(1, 129))
+        V = int(rng.choice([int(rng.integers(1, 300)), int(rng.integers(300, 5000)), int(rng.integers(5000, 40000))]))
+        density = float(rng.choice([1.0, 0.5, 0.02]))
         out.append((i, bf16, n, d, V, density))
     return out
 
