@@ -13,6 +13,9 @@
 //   lds        : random operands read from a 2-stage LDS ring every quarter
 //                with the kernel's swizzle, fragment mapping and read-ahead,
 //                one workgroup barrier per slice;
+//   lds_write  : as lds, plus the ring's write traffic alone: each wave
+//                writes its 8 x 1 KB of the stage just read from registers
+//                (ds_write_b128), no global reads;
 //   dma_l2     : as lds, plus the kernel's per-slice global -> LDS DMA of the
 //                stage just freed (8 x 1 KB per wave, 128-byte runs of rows
 //                4 KB apart) from a 4 MB source that stays in L2;
@@ -64,7 +67,7 @@ __global__ void fill_random(uint32_t* p, uint64_t n) {
 }
 
 // MODE 0 const, 1 random (registers only); 2 lds; 3 lds + DMA (the source
-// size decides L2 or HBM).
+// size decides L2 or HBM); 4 lds + register -> LDS writes of the same bytes.
 template <int MODE>
 __global__ __launch_bounds__(512, 1) void ceiling_kernel(const char* __restrict__ src, uint64_t n_regions,
                                                           float* out, int slices) {
@@ -138,7 +141,7 @@ __global__ __launch_bounds__(512, 1) void ceiling_kernel(const char* __restrict_
     }
     // slice boundary: wait for this wave's DMA, workgroup barrier, then the
     // DMA of the slice after next into the stage just read
-    if (MODE >= 3) asm volatile("s_waitcnt vmcnt(0)" ::: "memory");
+    if (MODE == 3) asm volatile("s_waitcnt vmcnt(0)" ::: "memory");
     if (MODE >= 2) asm volatile("s_waitcnt lgkmcnt(0)\n\ts_barrier" ::: "memory");
     if (MODE >= 2) {
       load_a(st ^ 1, 0, 0, fa[0]);
@@ -155,7 +158,11 @@ __global__ __launch_bounds__(512, 1) void ceiling_kernel(const char* __restrict_
 #pragma unroll
     for (int j = 0; j < 8; ++j) {
       mfma(fa[1][j / 4], fb[1][j % 4], acc[6 + j / 4][j % 4]);
-      if (MODE >= 3) {
+      if (MODE == 4) {
+        const int op = j / 4, blk = j % 4;
+        lds[st][op][(wave * 4 + blk) * 64 + lane] = fa[1][j & 1];
+      }
+      if (MODE == 3) {
         const int op = j / 4, blk = j % 4;
         dma16(sbase, off[blk],
               __builtin_amdgcn_readfirstlane(lds_base + static_cast<uint32_t>(((st * 2 + op) * kSlots +
@@ -211,18 +218,19 @@ int main() {
   const double c = measure<0>(src, 1, out, blocks, slices);
   const double r = measure<1>(src, 1, out, blocks, slices);
   const double l = measure<2>(src, 1, out, blocks, slices);
+  const double lw = measure<4>(src, 1, out, blocks, slices);
   const double d2 = measure<3>(src, small / kRegion, out, blocks, slices);
   const double dh = measure<3>(src, big / kRegion, out, blocks, slices);
   (void)hipFree(out);
   (void)hipFree(src);
-  if (c < 0 || r < 0 || l < 0 || d2 < 0 || dh < 0) {
+  if (c < 0 || r < 0 || l < 0 || lw < 0 || d2 < 0 || dh < 0) {
     std::fprintf(stderr, "kernel failed\n");
     return 1;
   }
   std::printf("{\"instruction\": \"v_mfma_f32_16x16x32_bf16\", \"cus\": %d, "
               "\"const_operands_tflops\": %.1f, \"random_operands_tflops\": %.1f, "
-              "\"slice_loop_lds_tflops\": %.1f, \"slice_loop_dma_l2_tflops\": %.1f, "
-              "\"slice_loop_dma_hbm_tflops\": %.1f}\n",
-              prop.multiProcessorCount, c, r, l, d2, dh);
+              "\"slice_loop_lds_tflops\": %.1f, \"slice_loop_lds_write_tflops\": %.1f, "
+              "\"slice_loop_dma_l2_tflops\": %.1f, \"slice_loop_dma_hbm_tflops\": %.1f}\n",
+              prop.multiProcessorCount, c, r, l, lw, d2, dh);
   return 0;
 }
