@@ -74,6 +74,7 @@ __device__ __forceinline__ void combine(float& m, float& s, float& z, float& t, 
 }
 
 static_assert(kKSteps == 2, "a K-slice is two K-steps");
+static_assert(kVB % 2 == 0, "the gradient epilogue pairs vocabulary blocks");
 
 // KTAIL: d is not a multiple of the K-slice, so the last slice of every
 // row needs zero-filling (a separate instantiation keeps that work out of the
@@ -353,8 +354,14 @@ __global__ __launch_bounds__(kThreads, 1) void lmhead_logprob_kernel(LmheadArgs 
   // wave, rounded to bf16.  In each block a lane holds 4 consecutive
   // vocabulary entries of its token row: half of an 8-entry chunk (lane
   // groups 0 and 1 hold the two halves of one chunk, groups 2 and 3 those of
-  // the next).  G is stored chunk-major, so one 8-byte store per block covers
-  // two runs of 256 contiguous bytes across the wave (16 token rows x one
+  // the next).  Blocks are taken in pairs: v_permlane16_swap_b32 trades the
+  // odd lane groups' halves of the first block for the even groups' halves
+  // of the second, so that every lane then holds one whole chunk, chunk
+  // frag_chunk(g) of the pair's four, and stores it with one 16-byte store
+  // (stores of 8 bytes per lane drained about 1.6 times slower: all work
+  // items reach this epilogue together, and the next K-slice's DMA wait
+  // also waits for these stores).  G is stored chunk-major, so a store
+  // instruction covers four runs of 256 contiguous bytes (16 token rows x one
   // chunk each).  Rows >= V hold -inf, so p = 0 and G = 0 there, which
   // zero-fills the columns up to g_cols.
   auto grad_epilogue = [&](int64_t vt) {
@@ -365,32 +372,42 @@ __global__ __launch_bounds__(kThreads, 1) void lmhead_logprob_kernel(LmheadArgs 
       const bool live = e < n_s;   // rows n_s .. round_up(n_s, 64) - 1 are written as zeros
       uint16_t* gcol = p.g_out + e * 8;   // chunk c of this row: gcol + c * g_ld * 8
       const float gneg = -g_up[bn];
+      // The sampled token's column gets g (1 - p), computed as g - g p (one
+      // rounding); `code` is its place 4 bm + q among this lane's elements of
+      // the column, -1 if the lane does not hold it.
+      const int o = tok[bn] - vbase;
+      const int code = (o >= 0 && o < 128 && ((o >> 2) & 3) == grp) ? (o >> 4) * 4 + (o & 3) : -1;
 #pragma unroll
-      for (int bm = 0; bm < kVB; ++bm) {
-        const int v0 = vbase + bm * 16 + 4 * grp;   // element q is column v0 + q
-        float gv[4];
+      for (int bp = 0; bp < kVB; bp += 2) {
+        uint32_t pk[2][2];   // [block of the pair][bf16 pair]: entries v0 .. v0 + 3
 #pragma unroll
-        for (int q = 0; q < 4; ++q)
-          gv[q] = gneg * fast_exp2(__builtin_fmaf(acc[bm][bn][q], kLog2e, -g_lse[bn]));
-        // The sampled token's column gets g (1 - p) instead: at most one
-        // element per row, so the branch is rarely taken by any lane.
-        const int dt = tok[bn] - v0;
-        if (static_cast<unsigned>(dt) < 4u) {
+        for (int h = 0; h < 2; ++h) {
+          const int bm = bp + h;
+          float gv[4];
 #pragma unroll
-          for (int q = 0; q < 4; ++q)
-            if (q == dt) gv[q] = g_up[bn] * (1.f - fast_exp2(__builtin_fmaf(acc[bm][bn][q], kLog2e, -g_lse[bn])));
+          for (int q = 0; q < 4; ++q) {
+            const float pv = fast_exp2(__builtin_fmaf(acc[bm][bn][q], kLog2e, -g_lse[bn]));
+            gv[q] = __builtin_fmaf(gneg, pv, code == bm * 4 + q ? g_up[bn] : 0.f);
+          }
+#pragma unroll
+          for (int r = 0; r < 4; r += 2) {
+            const uint32_t w = __builtin_bit_cast(uint32_t, __builtin_convertvector(f32x2_t{gv[r], gv[r + 1]}, bf16x2_t));
+            pk[h][r / 2] = live ? w : 0u;
+          }
         }
-        uint32_t pk[2];
-#pragma unroll
-        for (int r = 0; r < 4; r += 2) {
-          const uint32_t w = static_cast<uint32_t>(__builtin_bit_cast(uint16_t, static_cast<__bf16>(gv[r]))) |
-                             (static_cast<uint32_t>(__builtin_bit_cast(uint16_t, static_cast<__bf16>(gv[r + 1])))
-                              << 16);
-          pk[r / 2] = live ? w : 0u;
-        }
-        // entries v0 .. v0 + 3 = bytes 8 (grp & 1) .. + 7 of chunk v0 / 8
-        if (e < n_s_pad && vbase + bm * 16 < p.g_cols)
-          *reinterpret_cast<uint2*>(gcol + (v0 / 8) * p.g_ld * 8 + 4 * (grp & 1)) = make_uint2(pk[0], pk[1]);
+        // even lane groups keep their first-block half and receive the
+        // partner's (the chunk's upper half); odd groups receive the
+        // partner's second-block half (the lower half) and keep their own
+        const auto s0 = __builtin_amdgcn_permlane16_swap(pk[0][0], pk[1][0], false, false);
+        const auto s1 = __builtin_amdgcn_permlane16_swap(pk[0][1], pk[1][1], false, false);
+        const int chunk = (vbase + bp * 16) / 8 + frag_chunk(grp);
+        // (the pair's 32 columns lie wholly below g_cols, a multiple of 64, or
+        // wholly above).  Non-temporal: G is read back only by the two GEMMs,
+        // long after it has left the L2, and these write-backs would
+        // otherwise evict the tiles the next K-slices' DMAs read.
+        if (e < n_s_pad && vbase + bp * 16 < p.g_cols)
+          __builtin_nontemporal_store(u32x4_t{s0[0], s1[0], s0[1], s1[1]},
+                                      reinterpret_cast<u32x4_t*>(gcol + static_cast<int64_t>(chunk) * p.g_ld * 8));
       }
     }
 #pragma unroll

@@ -187,3 +187,43 @@ def test_fused_fragment_reads_are_bank_conflict_free():
     for R in range(0, 256, 32):
         for kk in range(4):
             assert pass_conflicts([frag32_slot(R, kk, l) for l in range(64)]) == 1
+
+
+# Gradient-mode G stores (lmhead_logprob.hip, gradient epilogue).  In a
+# 16 x 16 result block lane l holds token column l mod 16 and the 4
+# consecutive vocabulary rows 4 (l div 16) .. + 3 of the block.  Blocks are
+# paired (bm, bm + 1) and v_permlane16_swap_b32 is applied to each packed
+# word (first block's word as the first operand, second block's as the
+# second).  Its lane mapping, as measured on the GPU: within each pair of
+# 16-lane rows (0, 1) and (2, 3), lane i of the even row returns (its own
+# first operand, the first operand of lane i + 16), and lane i + 16 of the
+# odd row returns (the second operand of lane i, its own second operand).
+
+
+def permlane16_swap(first, second):
+    """Per-lane results (new first, new second) of v_permlane16_swap_b32."""
+    out = []
+    for l in range(64):
+        if (l >> 4) % 2 == 0:
+            out.append((first[l], first[l + 16]))
+        else:
+            out.append((second[l - 16], second[l]))
+    return out
+
+
+def test_grad_store_pairs_deliver_whole_chunks():
+    # word r (0, 1) of a lane's block holds the vocabulary rows 2 r, 2 r + 1
+    # of its four; after the swaps lane group g must hold, in order, the 8
+    # rows of chunk SIGMA[g] of the pair's four (chunks of 8 rows, counted
+    # from the pair's first row) for its own token column.
+    def word(l, h, r):
+        v0 = 16 * h + 4 * (l >> 4)   # first row of lane l in block h of the pair
+        return ((l & 15), (v0 + 2 * r, v0 + 2 * r + 1))
+
+    s = [permlane16_swap([word(l, 0, r) for l in range(64)], [word(l, 1, r) for l in range(64)]) for r in range(2)]
+    for l in range(64):
+        stored = [s[0][l][0], s[1][l][0], s[0][l][1], s[1][l][1]]
+        assert all(col == (l & 15) for col, _ in stored)
+        rows = [v for _, pair in stored for v in pair]
+        chunk = SIGMA[l >> 4]
+        assert rows == list(range(8 * chunk, 8 * chunk + 8)), (l, rows)
