@@ -222,6 +222,11 @@ __global__ __launch_bounds__(kThreads, 1) void gemm_kernel(GemmArgs p) {
   // ---- work item: XCD-aware (m-tile, n-tile, split) ----------------------
   // The j-th workgroup of an XCD belongs to launch group j / 32 of that XCD;
   // a group is gm x gn tiles of one split, sharing A and B rows through L2.
+  // Consecutive groups (which run at the same time on neighbouring XCDs)
+  // take the n-groups of one m-group first, so the XCDs that read the same
+  // rows of A (the large logit gradient) read them together and all but the
+  // first find them in the memory-side cache (3.7 % faster at c2 than
+  // m-groups first).
   const int64_t b = blockIdx.x;
   const int64_t xcd = b % kNumXcd;
   const int64_t j = b / kNumXcd;
@@ -233,8 +238,8 @@ __global__ __launch_bounds__(kThreads, 1) void gemm_kernel(GemmArgs p) {
   // wave-uniform results back in scalar registers for the DMA base)
   const int64_t split = __builtin_amdgcn_readfirstlane(static_cast<int>(grp_id / (n_gm * n_gn)));
   const int64_t rem = grp_id % (n_gm * n_gn);
-  const int64_t tm = __builtin_amdgcn_readfirstlane(static_cast<int>((rem % n_gm) * p.gm + loc % p.gm));
-  const int64_t tn = __builtin_amdgcn_readfirstlane(static_cast<int>((rem / n_gm) * p.gn + loc / p.gm));
+  const int64_t tm = __builtin_amdgcn_readfirstlane(static_cast<int>((rem / n_gn) * p.gm + loc % p.gm));
+  const int64_t tn = __builtin_amdgcn_readfirstlane(static_cast<int>((rem % n_gn) * p.gn + loc / p.gm));
   if (split >= p.splits || tm >= p.tiles_m || tn >= p.tiles_n) return;
 
   int64_t m_valid = p.m, k_valid = p.k;
