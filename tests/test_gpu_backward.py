@@ -81,6 +81,21 @@ def test_backward_several_chunks(hdl):
     _check(dw, want_dw, mag_dw, "dW")
 
 
+def test_backward_trailing_chunks_empty(hdl):
+    # 100,000 rows are planned as four chunks of 32,768 before the mask is
+    # known (the host never reads the scored count); a sparse mask leaves
+    # about 20,000 scored rows, so chunks 1-3 find no rows: their launches
+    # must leave dH and the dW already accumulated from chunk 0 untouched
+    H, W, y, m, up = _case(100000, 64, 300, seed=41, mask_p=0.2)
+    assert int(m.sum()) < 32768
+    dh, dw = _gpu(hdl, H, W, y, m, up)
+    want_dh, want_dw, mag_dh, mag_dw = O.token_logprobs_backward(as_f64(H), as_f64(W), y.numpy(),
+                                                                 up.double().numpy(), m.numpy())
+    _check(dh, want_dh, mag_dh, "dH")
+    _check(dw, want_dw, mag_dw, "dW")
+    assert np.all(dh[m.numpy() == 0] == 0.0)
+
+
 def test_backward_workload_shapes(hdl):
     # reduced agent workload (observation spans masked), original context only
     w = workloads.make_workload("c4", R=2, T=600, d=128, V=9000)
