@@ -240,6 +240,25 @@ def test_select_ties_at_boundary_take_lower_index(hdl):
     assert score[0].tolist() == [2.0, 1.0, 1.0, 1.0]
 
 
+@pytest.mark.parametrize("R,T,k", [(3, 20000, 8), (2, 20000, 700), (2, 40000, 64), (2, 40000, 1024), (4, 777, 65)])
+def test_select_many_ties_at_the_threshold(hdl, R, T, k):
+    # scores from five levels only, so the k-th place falls inside a large
+    # block of exact ties spread over every part of the root (staged roots
+    # and, for T > 32768, roots read again from global memory)
+    g = np.random.default_rng(T + k)
+    lo = np.full((R, T), -3.0, np.float32)
+    level = g.choice(5, size=(R, T), p=[0.4, 0.3, 0.2, 0.0998, 0.0002])   # s = level / 4
+    lh = (lo + 0.25 * level).astype(np.float32)
+    mask = (g.random((R, T)) < 0.9).astype(np.uint8)
+    idx, score, count, _ = hdl.select_branch_points(torch.from_numpy(lo).cuda(), torch.from_numpy(lh).cuda(),
+                                                    torch.from_numpy(mask).cuda(), k)
+    torch.cuda.synchronize()
+    oi, osc, oc = O.select_branch_points(lo, lh, mask, k, precision="f32")
+    assert np.array_equal(count.cpu().numpy(), oc)
+    assert np.array_equal(idx.cpu().numpy(), oi)
+    assert np.array_equal(score.cpu().numpy(), osc.astype(np.float32))
+
+
 def test_select_fewer_candidates_than_k(hdl):
     lo = np.array([[-1.0, -2.0, -3.0, -4.0]], np.float32)
     lh = np.array([[-1.5, np.nan, -1.0, -9.0]], np.float32)
