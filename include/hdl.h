@@ -330,9 +330,9 @@ int hdl_abi_version(void);
 
 /*
  * Kernel timing for measurement tools.  While enabled, every
- * hdl_token_logprobs(_entropy) call brackets its fused lm-head kernel, and
- * every hdl_token_logprobs_backward call its gradient-mode and GEMM launches,
- * with HIP events on the caller's stream.  hdl_profile_read waits for those
+ * hdl_token_logprobs(_entropy) call brackets its fused lm-head kernel, every
+ * hdl_token_logprobs_backward call its gradient-mode and GEMM launches, and
+ * every selection call its kernel, with HIP events on the caller's stream.  hdl_profile_read waits for those
  * events, returns the summed time of the fused kernel's launches in
  * milliseconds and their number since the last read, and resets that tally.
  * Disabled by default; enabling adds two event records per timed launch.
@@ -343,8 +343,9 @@ int hdl_profile_read(double* total_ms, int64_t* launches);
 
 /* The same tally for one kind of kernel: the fused lm-head kernel (what
  * hdl_profile_read reports), its gradient mode in hdl_token_logprobs_backward,
- * or the backward pass's GEMMs. */
-enum { HDL_PROFILE_LMHEAD = 0, HDL_PROFILE_GRAD = 1, HDL_PROFILE_GEMM = 2 };
+ * the backward pass's GEMMs, or the per-root selection kernel of
+ * hdl_select_branch_points, hdl_select_top_k and hdl_select_constrained. */
+enum { HDL_PROFILE_LMHEAD = 0, HDL_PROFILE_GRAD = 1, HDL_PROFILE_GEMM = 2, HDL_PROFILE_SELECT = 3 };
 int hdl_profile_read_kind(int kind, double* total_ms, int64_t* launches);
 
 #ifdef __cplusplus

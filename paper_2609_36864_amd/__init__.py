@@ -493,12 +493,13 @@ def profile_enable(on: bool = True) -> None:
     _check(load_library().hdl_profile_enable(1 if on else 0))
 
 
-PROFILE_LMHEAD, PROFILE_GRAD, PROFILE_GEMM = 0, 1, 2
+PROFILE_LMHEAD, PROFILE_GRAD, PROFILE_GEMM, PROFILE_SELECT = 0, 1, 2, 3
 
 
 def profile_read(kind: int = PROFILE_LMHEAD) -> Tuple[float, int]:
     """(summed milliseconds, launches) of one kernel kind since its last read:
-    the fused lm-head kernel (default), its gradient mode, or the backward GEMMs."""
+    the fused lm-head kernel (default), its gradient mode, the backward GEMMs,
+    or the per-root selection kernel."""
     ms = ctypes.c_double(0.0)
     n = ctypes.c_int64(0)
     _check(load_library().hdl_profile_read_kind(int(kind), ctypes.byref(ms), ctypes.byref(n)))

@@ -49,8 +49,9 @@ size_t round_up(size_t x, size_t a) { return (x + a - 1) / a * a; }
 
 // ---- kernel timing (measurement tools only) ------------------------------
 // Kinds: HDL_PROFILE_LMHEAD (fused lm-head kernel, statistics or entropy),
-// HDL_PROFILE_GRAD (its gradient mode), HDL_PROFILE_GEMM (backward GEMMs).
-constexpr int kProfileKinds = 3;
+// HDL_PROFILE_GRAD (its gradient mode), HDL_PROFILE_GEMM (backward GEMMs),
+// HDL_PROFILE_SELECT (the per-root selection kernel).
+constexpr int kProfileKinds = 4;
 using EventPair = std::pair<hipEvent_t, hipEvent_t>;
 struct Profiler {
   std::mutex mu;
@@ -296,9 +297,14 @@ int hdl_select_branch_points(const float* logp_orig, const float* logp_hind, con
     return fail(HDL_ERR_UNSUPPORTED, "hdl_select_branch_points: k=%d exceeds %d", k, HDL_MAX_K);
   if (n_roots > INT32_MAX || T > INT32_MAX)
     return fail(HDL_ERR_UNSUPPORTED, "hdl_select_branch_points: n_roots and T must fit in int32");
-  hipError_t e = hdl::launch_select(logp_orig, logp_hind, mask, n_roots, T, k, idx, score, count,
-                                    delta_signed, false, static_cast<hipStream_t>(stream));
+  const hipStream_t s = static_cast<hipStream_t>(stream);
+  TimedLaunch tl;
+  hipError_t e = tl.start(s);
+  if (e != hipSuccess) return hip_fail(e, "timing event");
+  e = hdl::launch_select(logp_orig, logp_hind, mask, n_roots, T, k, idx, score, count, delta_signed,
+                         false, s);
   if (e != hipSuccess) return hip_fail(e, "selection kernel launch");
+  if ((e = tl.stop(HDL_PROFILE_SELECT, s)) != hipSuccess) return hip_fail(e, "timing event");
   return HDL_OK;
 }
 
@@ -313,9 +319,13 @@ int hdl_select_top_k(const float* values, const uint8_t* mask, int64_t n_roots, 
   if (k > HDL_MAX_K) return fail(HDL_ERR_UNSUPPORTED, "hdl_select_top_k: k=%d exceeds %d", k, HDL_MAX_K);
   if (n_roots > INT32_MAX || T > INT32_MAX)
     return fail(HDL_ERR_UNSUPPORTED, "hdl_select_top_k: n_roots and T must fit in int32");
-  hipError_t e = hdl::launch_select(values, nullptr, mask, n_roots, T, k, idx, score, count, nullptr,
-                                    true, static_cast<hipStream_t>(stream));
+  const hipStream_t s = static_cast<hipStream_t>(stream);
+  TimedLaunch tl;
+  hipError_t e = tl.start(s);
+  if (e != hipSuccess) return hip_fail(e, "timing event");
+  e = hdl::launch_select(values, nullptr, mask, n_roots, T, k, idx, score, count, nullptr, true, s);
   if (e != hipSuccess) return hip_fail(e, "selection kernel launch");
+  if ((e = tl.stop(HDL_PROFILE_SELECT, s)) != hipSuccess) return hip_fail(e, "timing event");
   return HDL_OK;
 }
 
@@ -603,9 +613,14 @@ int hdl_select_constrained(const float* a, const float* b, const uint8_t* mask, 
     return fail(HDL_ERR_UNSUPPORTED, "%s: n_roots and T must fit in int32", fn);
   if (min_gap < 0) return fail(HDL_ERR_INVALID_ARG, "%s: min_gap=%d must be >= 0", fn, min_gap);
   const int pool = refill ? HDL_MAX_K : k;
-  hipError_t e = hdl::launch_select(a, b, mask, n_roots, T, k, idx, score, count, nullptr, b == nullptr,
-                                    static_cast<hipStream_t>(stream), lo, hi, min_gap, pool);
+  const hipStream_t s = static_cast<hipStream_t>(stream);
+  TimedLaunch tl;
+  hipError_t e = tl.start(s);
+  if (e != hipSuccess) return hip_fail(e, "timing event");
+  e = hdl::launch_select(a, b, mask, n_roots, T, k, idx, score, count, nullptr, b == nullptr, s, lo,
+                         hi, min_gap, pool);
   if (e != hipSuccess) return hip_fail(e, "selection kernel launch");
+  if ((e = tl.stop(HDL_PROFILE_SELECT, s)) != hipSuccess) return hip_fail(e, "timing event");
   return HDL_OK;
 }
 

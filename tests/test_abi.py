@@ -186,3 +186,15 @@ def test_noalloc_argument_checks_before_any_hip_call(lib):
     # 3 million rows of d = 8 would need 48 MB of the library's 32 MiB array
     assert f(p, p, p, None, 3_000_000, 8, 1000, 1, p, None, None) == -2
     assert b"scratch" in lib.hdl_last_hip_error()
+
+
+def test_profile_kinds(lib):
+    # every timing kind the header names reads back (nothing pending: zero
+    # launches, no HIP call); kinds outside the enumeration are rejected
+    ms = ctypes.c_double(-1.0)
+    n = ctypes.c_int64(-1)
+    for kind in (hdl.PROFILE_LMHEAD, hdl.PROFILE_GRAD, hdl.PROFILE_GEMM, hdl.PROFILE_SELECT):
+        assert lib.hdl_profile_read_kind(kind, ctypes.byref(ms), ctypes.byref(n)) == 0
+        assert n.value == 0 and ms.value == 0.0
+    for kind in (-1, 4):
+        assert lib.hdl_profile_read_kind(kind, ctypes.byref(ms), ctypes.byref(n)) < 0
