@@ -153,7 +153,7 @@ def _values_case(R, T, seed):
 
 
 @pytest.mark.parametrize("R,T,k", [(1, 1, 1), (3, 257, 2), (8, 4096, 8), (2, 9000, 64),
-                                   (5, 300, 1024)])
+                                   (5, 300, 1024), (2, 40000, 16), (1, 33000, 700)])
 def test_select_top_k_bit_exact_vs_oracle(hdl, R, T, k):
     v, mask = _values_case(R, T, seed=R * 31 + T + k)
     for m in (mask, None):

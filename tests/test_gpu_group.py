@@ -38,6 +38,8 @@ def _t(x, dtype=None):
     (8, 4096, 2, 64, True, True),
     (3, 5000, 16, 100, True, True),
     (2, 2000, 300, 3, True, False),
+    (2, 40000, 8, 500, True, True),    # longer than the LDS holds: read again from memory
+    (2, 33000, 100, 10, False, True),
 ])
 def test_constrained_selection_bit_exact(hdl, R, T, k, gap, refill, ranged):
     lo_, hi_, mask = workloads.make_logp_pair(R, T, seed=R * 7 + T + k + gap, nan_rows=1)
