@@ -304,7 +304,7 @@ __global__ __launch_bounds__(kThreads, 1) void gemm_kernel(GemmArgs p) {
 #pragma unroll
       for (int jj = 0; jj < 2; ++jj)
 #pragma unroll
-        for (int bn = 0; bn < kTB; ++bn) M::run(fa_[jj], fb_[bn], acc[2 * pr + jj][bn]);
+        for (int i = 0; i < kTB; ++i) M::run(fa_[jj], fb_[snake(jj, i)], acc[2 * pr + jj][snake(jj, i)]);
     };
 
     const int n_pre = n_iter < kStages ? n_iter : kStages;
@@ -355,7 +355,7 @@ __global__ __launch_bounds__(kThreads, 1) void gemm_kernel(GemmArgs p) {
       static_assert(kM == kDmaPerSlice, "one DMA per MFMA of the last quarter");
 #pragma unroll
       for (int q = 0; q < kM; ++q) {
-        M::run(fa[1][q / kTB], fb[1][q % kTB], acc[6 + q / kTB][q % kTB]);
+        M::run(fa[1][q / kTB], fb[1][snake(q / kTB, q % kTB)], acc[6 + q / kTB][snake(q / kTB, q % kTB)]);
         issue_one(q);
       }
     }

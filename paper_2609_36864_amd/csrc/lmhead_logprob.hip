@@ -278,7 +278,7 @@ __global__ __launch_bounds__(kThreads, 1) void lmhead_logprob_kernel(LmheadArgs 
 #pragma unroll
     for (int j = 0; j < 2; ++j)
 #pragma unroll
-      for (int bn = 0; bn < kTB; ++bn) M::run(a[j], b[bn], acc[2 * pr + j][bn]);
+      for (int i = 0; i < kTB; ++i) M::run(a[j], b[snake(j, i)], acc[2 * pr + j][snake(j, i)]);
   };
 
   // Online max / sum-of-exp update of one V-tile, then capture of the
@@ -491,7 +491,7 @@ __global__ __launch_bounds__(kThreads, 1) void lmhead_logprob_kernel(LmheadArgs 
         constexpr int kEvery = kM / kDmaPerSlice > 0 ? kM / kDmaPerSlice : 1;
 #pragma unroll
         for (int j = 0; j < kM; ++j) {
-          M::run(fa[1][j / kTB], fb[1][j % kTB], acc[6 + j / kTB][j % kTB]);
+          M::run(fa[1][j / kTB], fb[1][snake(j / kTB, j % kTB)], acc[6 + j / kTB][snake(j / kTB, j % kTB)]);
           if (j % kEvery == kEvery - 1 && j / kEvery < kDmaPerSlice) issue_one(j / kEvery, std::false_type{});
         }
 #pragma unroll

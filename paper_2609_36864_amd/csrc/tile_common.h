@@ -113,6 +113,15 @@ template <> struct Mma16<false> {
   }
 };
 
+// Order of the MFMAs of a quarter (two A fragments j = 0, 1 times kTB B
+// fragments): B fragment snake(j, i) is the i-th for A fragment j, i.e.
+// 0 .. kTB-1 for the first and kTB-1 .. 0 for the second, so that the B
+// operand is the same on both sides of the change of A and fewer operand
+// bits switch between consecutive MFMAs (with random data the matrix pipes
+// then sustain about 2 % more under the power limit).  The accumulator
+// blocks are independent, so the order does not change any result.
+__device__ __forceinline__ constexpr int snake(int j, int i) { return (j & 1) ? kTB - 1 - i : i; }
+
 // Which of a K-step's four 16-byte chunks lane group g reads: (0, 2, 1, 3).
 // A ds_read_b128 serves lanes i..i+7 together with lanes i+32..i+39, i.e.
 // lane groups g and g + 2 of the same 8 rows; they must read chunks c and

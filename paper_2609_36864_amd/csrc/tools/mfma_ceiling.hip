@@ -99,11 +99,16 @@ __global__ __launch_bounds__(512, 1) void ceiling_kernel(const char* __restrict_
     c = __builtin_amdgcn_mfma_f32_16x16x32_bf16(__builtin_bit_cast(bf16x8_t, a), __builtin_bit_cast(bf16x8_t, b), c,
                                                 0, 0, 0);
   };
+  // (the kernel's MFMA order: B fragments 0..3 with the first A fragment,
+  // 3..0 with the second)
   auto quarter = [&](const uint4 (&a)[2], const uint4 (&b)[4], int pr) {
 #pragma unroll
     for (int j = 0; j < 2; ++j)
 #pragma unroll
-      for (int bn = 0; bn < 4; ++bn) mfma(a[j], b[bn], acc[2 * pr + j][bn]);
+      for (int i = 0; i < 4; ++i) {
+        const int bn = j ? 3 - i : i;
+        mfma(a[j], b[bn], acc[2 * pr + j][bn]);
+      }
   };
   const uint32_t lds_base = static_cast<uint32_t>(
       reinterpret_cast<size_t>((__attribute__((address_space(3))) uint4*)(&lds[0][0][0])));
@@ -157,7 +162,8 @@ __global__ __launch_bounds__(512, 1) void ceiling_kernel(const char* __restrict_
                            ((static_cast<uint64_t>(blockIdx.x) + it) % n_regions) * kRegion;
 #pragma unroll
     for (int j = 0; j < 8; ++j) {
-      mfma(fa[1][j / 4], fb[1][j % 4], acc[6 + j / 4][j % 4]);
+      const int bn = (j / 4) ? 3 - j % 4 : j % 4;
+      mfma(fa[1][j / 4], fb[1][bn], acc[6 + j / 4][bn]);
       if (MODE == 4) {
         const int op = j / 4, blk = j % 4;
         lds[st][op][(wave * 4 + blk) * 64 + lane] = fa[1][j & 1];
